@@ -1,0 +1,132 @@
+"""Pins of the oracle's host policy against numbers the paper prints.
+
+  - Table 3 (App. B.1): single-token decode-time breakdown (FFN / QKVO /
+    attention / LM head) of Qwen2.5-7B, Qwen2.5-14B and Llama3.1-8B on an A100
+    (312 TFLOP/s fp16, 2.039 TB/s), each component max(compute, memory).
+    The printed shares include a small "nonlinear" column we do not model;
+    our four shares are scaled by (100 - nonlinear)/100 before comparing.
+  - Table 4 (App. B.3): idealized memory-bound T_q/T_p of 0.360 (W4) and
+    0.573 (W8) for Qwen2.5-7B at B = 1, S = 2k.
+  - App. D.2: W_D/W_T of a W4 drafter is about 33-36% of the target.
+  - Table 2 / App. E.2: alpha recovered from tau by inverting
+    tau = (1 - alpha^(gamma+1))/(1 - alpha).
+  - App. F.3: the gamma schedules 5->7->9->11 (Qwen2.5-7B, tau 5.73, 7.60,
+    9.48), 5->7->9 (Qwen2.5-14B, 5.73, 7.61), and Llama3.1-8B holding at 5
+    with tau ~ 5.5; no lowering at gamma_low.
+Model shapes are the public architectures of the three checkpoints.
+"""
+import numpy as np
+import pytest
+
+import oracle
+
+MODELS = {  # L, hidden, n_q, n_kv, head_dim, ffn, vocab
+    "qwen2.5-7b": (28, 3584, 28, 4, 128, 18944, 152064),
+    "qwen2.5-14b": (48, 5120, 40, 8, 128, 13824, 152064),
+    "llama3.1-8b": (32, 4096, 32, 8, 128, 14336, 128256),
+}
+
+TABLE3 = {  # (S, B): FFN, QKVO, Attn, LM head, Nonlinear (percent)
+    "qwen2.5-7b": {(2048, 8): (75.2, 10.9, 6.2, 7.2, 0.5), (2048, 4): (77.8, 11.2, 3.2, 7.4, 0.3),
+                   (4096, 2): (77.9, 11.2, 3.2, 7.4, 0.2), (8192, 1): (78.0, 11.2, 3.2, 7.5, 0.1)},
+    "qwen2.5-14b": {(2048, 8): (65.0, 19.3, 10.3, 5.0, 0.4), (2048, 4): (68.7, 20.4, 5.4, 5.2, 0.2),
+                    (4096, 2): (68.8, 20.4, 5.4, 5.3, 0.1), (8192, 1): (68.8, 20.4, 5.4, 5.3, 0.1)},
+    "llama3.1-8b": {(2048, 8): (65.4, 15.6, 12.4, 6.1, 0.5), (2048, 4): (69.9, 16.7, 6.7, 6.5, 0.3),
+                    (4096, 2): (70.0, 16.7, 6.7, 6.5, 0.2), (8192, 1): (70.0, 16.7, 6.7, 6.5, 0.1)},
+}
+
+
+@pytest.mark.parametrize("model", list(MODELS))
+def test_table3_decode_breakdown(model):
+    for (S, B), row in TABLE3[model].items():
+        t = oracle.decode_breakdown(*MODELS[model], B=B, S=S)
+        share = 100 * t / t.sum() * (100 - row[4]) / 100
+        assert np.all(np.abs(share - np.array(row[:4])) <= 0.15), (model, S, B, share)
+
+
+def test_table4_idealized_draft_ratio():
+    for dbits, printed in ((4, 0.360), (8, 0.573)):
+        c = oracle.cost_arch(*MODELS["qwen2.5-7b"], dbits=dbits, BW_eff=1.0, F_eff=1e30)
+        tp, tq, tv = oracle.cost_times(c, 1, 2048, 5)
+        assert abs(tq / tp - printed) <= 0.003, (dbits, tq / tp)
+
+
+def test_drafter_size_ratio():
+    for m, a in MODELS.items():
+        c = oracle.cost_arch(*a, dbits=4)
+        assert 0.32 <= c.W_D / c.W_T <= 0.36, (m, c.W_D / c.W_T)
+
+
+def test_tau_alpha_closed_form_and_inverse():
+    assert oracle.tau_from_alpha(0.0, 5) == pytest.approx(1.0)
+    assert oracle.tau_from_alpha(1.0, 5) == pytest.approx(6.0)
+    assert oracle.tau_from_alpha(0.9, 4) == pytest.approx((1 - 0.9 ** 5) / 0.1)
+    # brute force: tau is the expected count of a truncated geometric chain
+    rng = np.random.default_rng(0)
+    a, g = 0.8, 4
+    runs = rng.random((200_000, g)) < a
+    first_fail = np.where(~runs, np.arange(g), g).min(axis=1)
+    assert abs((first_fail + 1).mean() - oracle.tau_from_alpha(a, g)) < 0.02
+    for alpha in (0.3, 0.85, 0.97):
+        for gamma in (3, 5, 11):
+            assert oracle.alpha_from_tau(oracle.tau_from_alpha(alpha, gamma), gamma) == pytest.approx(alpha, abs=1e-9)
+
+
+@pytest.mark.parametrize("tau,gamma,alpha_pct", [
+    (7.5, 7, 98.2), (5.6, 5, 97.3), (5.5, 5, 96.3), (2.1, 3, 57.3), (5.4, 5, 95.8),
+])
+def test_table2_alpha_from_tau(tau, gamma, alpha_pct):
+    # tau is printed to one decimal: the printed alpha must lie in the image of [tau-0.05, tau+0.05]
+    lo = 100 * oracle.alpha_from_tau(tau - 0.05, gamma)
+    hi = 100 * oracle.alpha_from_tau(tau + 0.05, gamma)
+    assert lo - 0.05 <= alpha_pct <= hi + 0.05, (lo, hi)
+
+
+GSET = [5, 7, 9, 11]
+
+
+def _schedule(taus):
+    out, hist, g = [], [], GSET[0]
+    for t in taus:
+        hist.append(t)
+        g = oracle.gamma_next(GSET, g, hist, P=2, a_up=0.94, a_down=0.85)
+        out.append(g)
+    return out
+
+
+def test_app_f3_gamma_schedules():
+    # Qwen2.5-7B: tau reaches 5.73, 7.60, 9.48 before each raise
+    assert _schedule([5.0, 5.73, 5.73, 7.37, 7.60, 7.60, 9.35, 9.48, 9.48, 11.25]) == \
+        [5, 5, 7, 7, 7, 9, 9, 9, 11, 11]
+    # Qwen2.5-14B: 5.73 and 7.61
+    assert _schedule([5.73, 5.73, 7.61, 7.61])[-1] == 9
+    # Llama3.1-8B: tau improves from 5.07 to ~5.5 and never crosses 1 + 5*0.94 = 5.70
+    assert _schedule([5.07, 5.2, 5.3, 5.5, 5.5, 5.5]) == [5] * 6
+    # the raise needs the minimum of the window at or above 1 + gamma*alpha_up
+    assert _schedule([5.705, 5.705])[-1] == 7 and _schedule([5.695, 5.71])[-1] == 5
+    # lowering: max of the window <= 1 + gamma*alpha_down, never below gamma_low
+    assert oracle.gamma_next(GSET, 9, [7.0, 8.645], P=2) == 7
+    assert oracle.gamma_next(GSET, 9, [7.0, 8.655], P=2) == 9
+    assert oracle.gamma_next(GSET, 5, [2.0, 2.0], P=2) == 5
+    assert oracle.gamma_next(GSET, 11, [12.0, 12.0], P=2) == 11
+    # fewer than P measurements: hold
+    assert oracle.gamma_next(GSET, 5, [6.0], P=2) == 5
+
+
+def test_toggle_rule_and_monotonicity():
+    a = MODELS["llama3.1-8b"]
+    c = oracle.cost_arch(*a, BW_eff=1.6e12, F_eff=2.5e14, rho_kappa=0.8, eta_D=1.1, c_T=1e-5, c_D=1e-5, c_V=2e-5)
+    gamma, tau = 5, 5.2
+    sp = []
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+        tp, tq, tv = oracle.cost_times(c, B, 2048, gamma)
+        s = oracle.sd_speedup(tau, tp, tq, tv, gamma)
+        sp.append(s)
+        assert oracle.toggle(c, B, 2048, tau, gamma, 0.05) == int(s >= 1.05)
+    assert all(x >= y - 1e-12 for x, y in zip(sp, sp[1:])), sp   # speedup falls as the batch grows
+    assert sp[0] > 1.05 and sp[-1] < 1.0
+    # sticky: once on, a large batch does not switch it off
+    state = [0]
+    assert oracle.toggle_sticky(c, 512, 2048, tau, gamma, 0.05, state) == 0
+    assert oracle.toggle_sticky(c, 2, 2048, tau, gamma, 0.05, state) == 1
+    assert oracle.toggle_sticky(c, 512, 2048, tau, gamma, 0.05, state) == 1
