@@ -1,0 +1,116 @@
+"""Comparison of one device SD step against the oracle -- TEST INFRASTRUCTURE.
+
+The device side is given as numpy arrays copied back from the library; the
+oracle runs its own step on its own state (its inputs come only from the
+seeded generators and from its own earlier outputs).  Rules:
+
+  logits   max |dev - oracle| <= tol * max |oracle| per row (tol 5e-3 for
+           fp32 models, 2e-2 for bf16);
+  draws    a token drawn by exponential race must be identical unless the
+           oracle's two best keys are closer than twice the largest logit
+           difference of that row (then both draws are correct outcomes of
+           nearly equal keys and the sequence stops being compared);
+  accept   accept / reject decisions must be identical unless
+           |u - p/q| < 1e-3 at the deciding position; the final residual or
+           bonus draw follows the draw rule.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+
+class Mismatch(AssertionError):
+    pass
+
+
+def row_tol_ok(dev, ref, tol):
+    scale = np.abs(ref).max(axis=-1)
+    err = np.abs(dev - ref).max(axis=-1)
+    return bool(np.all(err <= tol * scale)), float((err / np.maximum(scale, 1e-30)).max())
+
+
+def compare_step(r: dict, dev: dict, tol: float, T: float = 1.0):
+    """r: oracle step (oracle.sd_step_seq); dev: draft, q, p, out, n_emit of
+    the same sequence from the device.  Returns ("ok" | "exempt", info);
+    raises Mismatch on a real disagreement."""
+    gamma = len(r["draft"])
+    worst = 0.0
+    for j in range(gamma):
+        ok, rel = row_tol_ok(dev["q"][j], r["q"][j], tol)
+        worst = max(worst, rel)
+        if not ok:
+            raise Mismatch(f"draft logits row {j}: rel err {rel:.3e} > {tol}")
+        if int(dev["draft"][j]) != int(r["draft"][j]):
+            delta = float(np.abs(dev["q"][j] - r["q"][j]).max()) / T
+            if r["draft_gap"][j] <= 2 * delta + 1e-6:
+                return "exempt", dict(where=f"draft {j}", gap=float(r["draft_gap"][j]), delta=delta, worst=worst)
+            raise Mismatch(f"draft token {j}: dev {dev['draft'][j]} oracle {r['draft'][j]} "
+                           f"gap {r['draft_gap'][j]:.3e} delta {delta:.3e}")
+    ok, rel = row_tol_ok(dev["p"], r["p"], tol)
+    worst = max(worst, rel)
+    if not ok:
+        raise Mismatch(f"verify logits: rel err {rel:.3e} > {tol}")
+    n_d, n_o = int(dev["n_emit"]), r["n_emit"]
+    out_d = np.asarray(dev["out"][:n_d])
+    if n_d == n_o and np.array_equal(out_d, r["out"]):
+        return "ok", dict(worst=worst)
+    # decisions differ: find the deciding position
+    k = min(n_d, n_o)               # 1-based position of the first differing decision
+    if k <= gamma and abs(float(r["u"][k - 1]) - float(r["ratio"][k - 1])) < 1e-3:
+        return "exempt", dict(where=f"accept {k}", u=float(r["u"][k - 1]), ratio=float(r["ratio"][k - 1]))
+    if n_d == n_o:
+        delta = float(np.abs(dev["p"] - r["p"]).max() + np.abs(dev["q"] - r["q"]).max()) / T
+        if r["final_gap"] <= 2 * delta + 1e-6:
+            return "exempt", dict(where="final draw", gap=r["final_gap"], delta=delta)
+    raise Mismatch(f"accept: dev n={n_d} out={out_d.tolist()} oracle n={n_o} out={r['out'].tolist()} "
+                   f"u={r['u'].tolist()} ratio={r['ratio'].tolist()}")
+
+
+def compare_ar(x_oracle: int, gap: float, p_oracle, x_dev: int, p_dev, tol: float, T: float = 1.0):
+    ok, rel = row_tol_ok(p_dev, p_oracle, tol)
+    if not ok:
+        raise Mismatch(f"AR logits: rel err {rel:.3e} > {tol}")
+    if x_dev == x_oracle:
+        return "ok"
+    delta = float(np.abs(p_dev - p_oracle).max()) / T
+    if gap <= 2 * delta + 1e-6:
+        return "exempt"
+    raise Mismatch(f"AR token: dev {x_dev} oracle {x_oracle} gap {gap:.3e} delta {delta:.3e}")
+
+
+def unpack_q4(packed: np.ndarray, scales_bits: np.ndarray, N: int, K: int):
+    """Codes [N][K] (int8) and scales [N][K/128] (fp16 bits) from the
+    library's packed tile layout (documented in include/sd_api.h)."""
+    G = K // 128
+    words = packed.view(np.uint32).reshape(N // 16, G, 64, 4)
+    codes = np.zeros((N, K), dtype=np.int8)
+    l = np.arange(64)
+    n_in = l % 16
+    c = l // 16
+    for j in range(4):
+        w = words[:, :, :, j]                       # [nb, g, lane]
+        for e in range(8):
+            nib = (w >> np.uint32(4 * (e // 2) + 16 * (e % 2))) & np.uint32(15)
+            k_in = 32 * j + 8 * c + e               # per lane
+            for g in range(G):
+                rows = (np.arange(N // 16)[:, None] * 16 + n_in[None, :])
+                codes[rows, g * 128 + k_in[None, :]] = nib[:, g, :].astype(np.int16) - 8
+    sc = scales_bits.view(np.uint16).reshape(N // 16, G, 16).transpose(0, 2, 1).reshape(N, G)
+    return codes, sc
+
+
+def drafter_layout(cfg: dict):
+    """(layer, which, N, K, code_offset, scale_offset) of every quantized
+    projection in the drafter buffer (include/sd_api.h)."""
+    H, d, F = cfg["hidden"], cfg["head_dim"], cfg["ffn"]
+    shapes = [((cfg["n_q"] + 2 * cfg["n_kv"]) * d, H), (H, cfg["n_q"] * d), (2 * F, H), (H, F)]
+    a256 = lambda x: (x + 255) // 256 * 256
+    out, off = [], 0
+    for l in range(cfg["n_layers"]):
+        for w, (N, K) in enumerate(shapes):
+            cb, sb = a256(N * K // 2), a256(N * (K // 128) * 2)
+            out.append((l, w, N, K, off, off + cb))
+            off += cb + sb
+    return out, off

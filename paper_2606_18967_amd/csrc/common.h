@@ -1,0 +1,77 @@
+// common.h -- shared device helpers for the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define WAVE 64
+
+// ------------------------------------------------------------ bf16 storage
+// bf16 values are stored as raw uint16_t bit patterns.
+struct bf16_t { uint16_t x; };
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Element access for the two model dtypes.
+template <typename T> struct elem;
+template <> struct elem<float> {
+    static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+    static __device__ __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+};
+template <> struct elem<uint16_t> {
+    static __device__ __forceinline__ float load(const uint16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+    static __device__ __forceinline__ void store(uint16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+// ------------------------------------------------------------ reductions
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+    return v;
+}
+
+// block-wide sum for blockDim.x a multiple of 64 (<= 1024); red has >= 16 floats
+__device__ __forceinline__ float block_sum(float v, float* red)
+{
+    int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) red[w] = v;
+    __syncthreads();
+    float t = 0.f;
+    for (int i = 0; i < nw; ++i) t += red[i];
+    return t;
+}
+
+// ------------------------------------------------------------ error flags
+// Device-side error words: a kernel that meets an out-of-range index sets its
+// word to 1 (plain vector store) and skips the work that would have gone out
+// of bounds.  The host reads the words back in sd_sync.
+enum : int {
+    ERR_SLOT = 0,       // slot index outside [0, max_slots)
+    ERR_TOKEN = 1,      // token id outside [0, vocab)
+    ERR_CTX = 2,        // a position at or beyond max_ctx
+    ERR_COUNT = 4
+};
+__device__ __forceinline__ void flag_error(uint32_t* err, int kind) { ((volatile uint32_t*)err)[kind] = 1u; }

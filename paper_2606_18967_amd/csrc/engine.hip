@@ -1,0 +1,453 @@
+// engine.hip -- the SD engine behind the C ABI (include/sd_api.h): bound
+// weights and KV, the engine-owned workspace, and the sequencing of one
+// forward pass / draft / verify / accept / rollback on a HIP stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/sd_api.h"
+#include "common.h"
+#include "kernels.h"
+
+// ------------------------------------------------------------------ errors
+static thread_local std::string g_err;
+
+static sd_status fail(sd_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+static sd_status fail(sd_status st, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+extern "C" const char* sd_last_error(void) { return g_err.c_str(); }
+
+#define HIP_TRY(call)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (call);                                                              \
+        if (e_ != hipSuccess) return fail(SD_E_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+static sd_status launched(const char* what)
+{
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(SD_E_HIP, "%s: kernel launch failed: %s", what, hipGetErrorString(e));
+    return SD_OK;
+}
+
+// ------------------------------------------------------------------ engine
+enum { PRJ_QKV = 0, PRJ_O = 1, PRJ_GU = 2, PRJ_DOWN = 3 };
+
+struct sd_engine_s {
+    sd_model_cfg c;
+    int max_slots, max_ctx, max_gamma, rows_max, max_chunks;
+    int dev;
+    bool f32;
+    int poison = 0;
+    // bound (caller-owned)
+    std::vector<const void*> w;
+    bool weights_bound = false;
+    void* k = nullptr;
+    void* v = nullptr;
+    int32_t* kv_len = nullptr;
+    std::vector<const uint32_t*> qw;   // [L*4] packed codes
+    std::vector<const uint16_t*> qs;   // [L*4] scales
+    bool drafter_ready = false;
+    // workspace (engine-owned)
+    float* h = nullptr;
+    void* a = nullptr;
+    float* qkv = nullptr;
+    float* qrot = nullptr;
+    void* att = nullptr;
+    float* gu = nullptr;
+    void* act = nullptr;
+    float* att_part = nullptr;
+    float* samp_part = nullptr;
+    float* acc_work = nullptr;
+    float2* rope = nullptr;
+    uint32_t* err = nullptr;
+};
+
+static void prj_shape(const sd_model_cfg& c, int which, int* N, int* K)
+{
+    int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
+    switch (which) {
+        case PRJ_QKV: *N = qkvN; *K = c.hidden; break;
+        case PRJ_O: *N = c.hidden; *K = c.n_q * c.head_dim; break;
+        case PRJ_GU: *N = 2 * c.ffn; *K = c.hidden; break;
+        default: *N = c.hidden; *K = c.ffn; break;
+    }
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static size_t prj_bytes(const sd_model_cfg& c, int which, size_t* codes, size_t* scales)
+{
+    int N, K;
+    prj_shape(c, which, &N, &K);
+    *codes = align256((size_t)N * K / 2);
+    *scales = align256((size_t)N * (K / 128) * 2);
+    return *codes + *scales;
+}
+
+static sd_status check_cfg(const sd_model_cfg* c)
+{
+    if (!c) return fail(SD_E_INVAL, "cfg is NULL");
+    if (c->n_layers < 1 || c->hidden < 1 || c->n_q < 1 || c->n_kv < 1 || c->ffn < 1 || c->vocab < 1)
+        return fail(SD_E_INVAL, "model dimensions must be positive");
+    if (c->dtype != SD_DTYPE_F32 && c->dtype != SD_DTYPE_BF16) return fail(SD_E_INVAL, "dtype must be F32 or BF16");
+    if (c->group != 128) return fail(SD_E_UNSUPPORTED, "group must be 128");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(SD_E_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->n_q % c->n_kv) return fail(SD_E_INVAL, "n_q must be a multiple of n_kv");
+    if (c->hidden % 128 || c->ffn % 128 || (c->n_q * c->head_dim) % 128)
+        return fail(SD_E_UNSUPPORTED, "hidden, ffn and n_q*head_dim must be multiples of 128");
+    if (((c->n_q + 2 * c->n_kv) * c->head_dim) % 64 || c->vocab % 64)
+        return fail(SD_E_UNSUPPORTED, "(n_q+2*n_kv)*head_dim and vocab must be multiples of 64");
+    if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return fail(SD_E_INVAL, "rms_eps and rope_theta must be > 0");
+    return SD_OK;
+}
+
+extern "C" int32_t sd_num_weights(const sd_model_cfg* c) { return c ? 3 + 6 * c->n_layers : -1; }
+
+extern "C" size_t sd_kv_bytes(const sd_model_cfg* c, int32_t max_slots, int32_t max_ctx)
+{
+    if (!c) return 0;
+    size_t el = c->dtype == SD_DTYPE_F32 ? 4 : 2;
+    return (size_t)c->n_layers * max_slots * c->n_kv * (size_t)max_ctx * c->head_dim * el;
+}
+
+extern "C" size_t sd_drafter_bytes(const sd_model_cfg* c)
+{
+    if (!c) return 0;
+    size_t total = 0, a, b;
+    for (int w = 0; w < 4; ++w) total += prj_bytes(*c, w, &a, &b);
+    return total * (size_t)c->n_layers;
+}
+
+static void free_ws(sd_engine e)
+{
+    void* ps[] = {e->h, e->a, e->qkv, e->qrot, e->att, e->gu, e->act, e->att_part, e->samp_part, e->acc_work, e->rope, e->err};
+    for (void* p : ps)
+        if (p) (void)hipFree(p);
+}
+
+extern "C" sd_status sd_create(const sd_model_cfg* cfg, int32_t max_slots, int32_t max_ctx, int32_t max_gamma,
+                               sd_engine* out)
+{
+    sd_status st = check_cfg(cfg);
+    if (st != SD_OK) return st;
+    if (!out) return fail(SD_E_INVAL, "out is NULL");
+    if (max_slots < 1 || max_ctx < 2 || max_gamma < 1 || max_gamma > 64)
+        return fail(SD_E_INVAL, "need max_slots >= 1, max_ctx >= 2, 1 <= max_gamma <= 64");
+    sd_engine e = new sd_engine_s();
+    e->c = *cfg;
+    e->max_slots = max_slots;
+    e->max_ctx = max_ctx;
+    e->max_gamma = max_gamma;
+    e->rows_max = max_slots * (max_gamma + 1);
+    e->max_chunks = (max_ctx + attention_chunk() - 1) / attention_chunk();
+    e->f32 = cfg->dtype == SD_DTYPE_F32;
+    e->w.assign(sd_num_weights(cfg), nullptr);
+    e->qw.assign(4 * cfg->n_layers, nullptr);
+    e->qs.assign(4 * cfg->n_layers, nullptr);
+    if (hipGetDevice(&e->dev) != hipSuccess) { delete e; return fail(SD_E_HIP, "hipGetDevice failed"); }
+
+    const sd_model_cfg& c = *cfg;
+    size_t R = (size_t)e->rows_max;
+    int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim, qd = c.n_q * c.head_dim;
+    struct { void** p; size_t bytes; } allocs[] = {
+        {(void**)&e->h, R * c.hidden * 4},
+        {(void**)&e->a, R * c.hidden * 4},
+        {(void**)&e->qkv, R * qkvN * 4},
+        {(void**)&e->qrot, R * qd * 4},
+        {(void**)&e->att, R * qd * 4},
+        {(void**)&e->gu, R * 2 * (size_t)c.ffn * 4},
+        {(void**)&e->act, R * c.ffn * 4},
+        {(void**)&e->att_part, attention_part_floats((int)R, c.n_q, c.head_dim, e->max_chunks) * 4},
+        {(void**)&e->samp_part, sample_part_floats((int)R, c.vocab) * 4},
+        {(void**)&e->acc_work, accept_work_floats(max_slots, max_gamma) * 4},
+        {(void**)&e->rope, (size_t)max_ctx * (c.head_dim / 2) * sizeof(float2)},
+        {(void**)&e->err, ERR_COUNT * 4},
+    };
+    for (auto& al : allocs) {
+        if (hipMalloc(al.p, al.bytes) != hipSuccess) {
+            free_ws(e);
+            delete e;
+            (void)hipGetLastError();
+            return fail(SD_E_NOMEM, "workspace allocation of %zu bytes failed", al.bytes);
+        }
+    }
+    // RoPE table: cos/sin(pos * theta^(-2i/d)) computed in double on the host
+    int hd = c.head_dim / 2;
+    std::vector<float2> tab((size_t)max_ctx * hd);
+    for (int p = 0; p < max_ctx; ++p)
+        for (int i = 0; i < hd; ++i) {
+            double ang = p * pow((double)c.rope_theta, -2.0 * i / c.head_dim);
+            tab[(size_t)p * hd + i] = make_float2((float)cos(ang), (float)sin(ang));
+        }
+    if (hipMemcpy(e->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemset(e->err, 0, ERR_COUNT * 4) != hipSuccess) {
+        free_ws(e);
+        delete e;
+        return fail(SD_E_HIP, "workspace initialisation failed");
+    }
+    *out = e;
+    return SD_OK;
+}
+
+extern "C" sd_status sd_destroy(sd_engine e)
+{
+    if (!e) return fail(SD_E_INVAL, "engine is NULL");
+    (void)hipDeviceSynchronize();
+    free_ws(e);
+    delete e;
+    return SD_OK;
+}
+
+extern "C" sd_status sd_bind_weights(sd_engine e, const void* const* t, int32_t n)
+{
+    if (!e || !t) return fail(SD_E_INVAL, "NULL argument");
+    if (n != sd_num_weights(&e->c)) return fail(SD_E_INVAL, "expected %d tensors, got %d", sd_num_weights(&e->c), n);
+    for (int i = 0; i < n; ++i)
+        if (!t[i]) return fail(SD_E_INVAL, "tensor %d is NULL", i);
+    for (int i = 0; i < n; ++i) e->w[i] = t[i];
+    e->weights_bound = true;
+    e->drafter_ready = false;   // quantized copy is stale until refreshed
+    return SD_OK;
+}
+
+extern "C" sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len)
+{
+    if (!e || !k || !v || !kv_len) return fail(SD_E_INVAL, "NULL argument");
+    e->k = k;
+    e->v = v;
+    e->kv_len = kv_len;
+    return SD_OK;
+}
+
+extern "C" sd_status sd_set_debug(sd_engine e, int32_t poison)
+{
+    if (!e) return fail(SD_E_INVAL, "engine is NULL");
+    e->poison = poison != 0;
+    return SD_OK;
+}
+
+static const void* W(sd_engine e, int layer, int idx) { return e->w[3 + 6 * layer + idx]; }
+
+extern "C" sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream)
+{
+    if (!e || !qbuf) return fail(SD_E_INVAL, "NULL argument");
+    if (!e->weights_bound) return fail(SD_E_STATE, "weights not bound");
+    if (bytes < sd_drafter_bytes(&e->c)) return fail(SD_E_INVAL, "qbuf holds %zu bytes, need %zu", bytes, sd_drafter_bytes(&e->c));
+    hipStream_t s = (hipStream_t)stream;
+    char* p = (char*)qbuf;
+    static const int widx[4] = {1, 2, 4, 5};   // Wqkv, Wo, Wgu, Wdown within a layer
+    for (int l = 0; l < e->c.n_layers; ++l)
+        for (int wh = 0; wh < 4; ++wh) {
+            int N, K;
+            size_t cb, sb;
+            prj_shape(e->c, wh, &N, &K);
+            prj_bytes(e->c, wh, &cb, &sb);
+            uint32_t* q = (uint32_t*)p;
+            uint16_t* sc = (uint16_t*)(p + cb);
+            launch_quant_rtn4(W(e, l, widx[wh]), e->f32, N, K, q, sc, s);
+            e->qw[4 * l + wh] = q;
+            e->qs[4 * l + wh] = sc;
+            p += cb + sb;
+        }
+    sd_status st = launched("sd_refresh_drafter");
+    if (st == SD_OK) e->drafter_ready = true;
+    return st;
+}
+
+// ------------------------------------------------------------------ forward
+static act_t act_of(sd_engine e, bool draft) { return e->f32 ? ACT_F32 : (draft ? ACT_F16 : ACT_BF16); }
+
+static void proj(sd_engine e, bool draft, int layer, int which, const void* A, float* C, int M, int ldc,
+                 gemm_mode mode, hipStream_t s)
+{
+    int N, K;
+    prj_shape(e->c, which, &N, &K);
+    static const int widx[4] = {1, 2, 4, 5};
+    if (draft) {
+        const uint32_t* q = e->qw[4 * layer + which];
+        const uint16_t* sc = e->qs[4 * layer + which];
+        if (e->f32) launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s);
+        else launch_gemm_q4_f16((const _Float16*)A, q, sc, C, M, N, K, ldc, mode, s);
+    } else {
+        const void* w = W(e, layer, widx[which]);
+        if (e->f32) launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s);
+        else launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, M, N, K, ldc, mode, s);
+    }
+}
+
+// One forward pass over B sequences x n tokens (row r = b*n + i at position
+// kv_len + off + i).  Token of row (b, i): i == 0 ? tokA[b*sA] :
+// tokB[b*sB + i - 1].  If logits != NULL, row r's logits go to logits + r*ldl.
+static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const int32_t* tokA, int sA,
+                    const int32_t* tokB, int sB, int n, int off, float* logits, long ldl, hipStream_t s)
+{
+    const sd_model_cfg& c = e->c;
+    rows_t r = {B, n, off, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
+    cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, c.n_kv, c.head_dim};
+    int R = B * n;
+    act_t at = act_of(e, draft);
+    int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
+    launch_embed(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, s);
+    for (int l = 0; l < c.n_layers; ++l) {
+        launch_rmsnorm(e->h, R, c.hidden, W(e, l, 0), e->f32, c.rms_eps, e->a, at, s);
+        proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s);
+        launch_rope_kv(r, e->qkv, e->rope, c.n_q, kv, l, e->qrot, s);
+        launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s);
+        proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s);
+        launch_rmsnorm(e->h, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s);
+        proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s);
+        launch_silu_mul(e->gu, R, c.ffn, e->act, at, s);
+        proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s);
+    }
+    if (logits) {
+        // the LM head stays in the target precision for the drafter too
+        act_t lt = e->f32 ? ACT_F32 : ACT_BF16;
+        launch_rmsnorm(e->h, R, c.hidden, e->w[1], e->f32, c.rms_eps, e->a, lt, s);
+        if (e->f32) launch_gemm_f32((const float*)e->a, (const float*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
+        else launch_gemm_bf16((const uint16_t*)e->a, (const uint16_t*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
+    }
+}
+
+static sd_status check_step(sd_engine e, int B, const void* slots, bool need_drafter)
+{
+    if (!e) return fail(SD_E_INVAL, "engine is NULL");
+    if (!slots) return fail(SD_E_INVAL, "slots is NULL");
+    if (B < 1 || B > e->max_slots) return fail(SD_E_INVAL, "B=%d outside [1, %d]", B, e->max_slots);
+    if (!e->weights_bound) return fail(SD_E_STATE, "weights not bound");
+    if (!e->kv_len) return fail(SD_E_STATE, "KV cache not bound");
+    if (need_drafter && !e->drafter_ready) return fail(SD_E_STATE, "drafter not refreshed");
+    return SD_OK;
+}
+
+extern "C" sd_status sd_prefill(sd_engine e, int32_t B, const int32_t* slots, const int32_t* tokens, int32_t n,
+                                void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if (!tokens || n < 1) return fail(SD_E_INVAL, "need tokens and n >= 1");
+    if (n > e->max_ctx) return fail(SD_E_INVAL, "n=%d exceeds max_ctx=%d", n, e->max_ctx);
+    hipStream_t s = (hipStream_t)stream;
+    int chunk = e->rows_max / B;
+    for (int t0 = 0; t0 < n; t0 += chunk) {
+        int nc = n - t0 < chunk ? n - t0 : chunk;
+        forward(e, false, B, slots, tokens + t0, n, tokens + t0 + 1, n, nc, 0, nullptr, 0, s);
+        launch_kv_advance(B, slots, nullptr, nc, e->kv_len, e->max_slots, e->err, s);
+    }
+    return launched("sd_prefill");
+}
+
+static sd_status check_gamma(sd_engine e, int gamma, float T)
+{
+    if (gamma < 1 || gamma > e->max_gamma) return fail(SD_E_INVAL, "gamma=%d outside [1, %d]", gamma, e->max_gamma);
+    if (!(T > 0.f) || !isfinite(T)) return fail(SD_E_INVAL, "temperature must be finite and > 0");
+    return SD_OK;
+}
+
+extern "C" sd_status sd_draft(sd_engine e, int32_t B, const int32_t* slots, const int32_t* last_tok, int32_t gamma,
+                              float T, sd_rng rng, int32_t* draft_tok, float* q_logits, float* q_stats, void* stream)
+{
+    sd_status st = check_step(e, B, slots, true);
+    if (st != SD_OK) return st;
+    if ((st = check_gamma(e, gamma, T)) != SD_OK) return st;
+    if (!last_tok || !draft_tok || !q_logits || !q_stats) return fail(SD_E_INVAL, "NULL buffer");
+    hipStream_t s = (hipStream_t)stream;
+    int V = e->c.vocab;
+    rows_t r = {B, 1, 0, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
+    rng_t rg = {rng.seed, rng.step};
+    long ld = (long)gamma * V;
+    for (int j = 1; j <= gamma; ++j) {
+        const int32_t* tok = j == 1 ? last_tok : draft_tok + (j - 2);
+        int stride = j == 1 ? 1 : gamma;
+        float* lg = q_logits + (size_t)(j - 1) * V;
+        forward(e, true, B, slots, tok, stride, tok, stride, 1, j - 1, lg, ld, s);
+        launch_sample(r, lg, ld, V, T, rg, j, draft_tok + (j - 1), gamma, q_stats + 2 * (j - 1), 2 * gamma,
+                      e->samp_part, s);
+    }
+    return launched("sd_draft");
+}
+
+extern "C" sd_status sd_verify(sd_engine e, int32_t B, const int32_t* slots, const int32_t* last_tok,
+                               const int32_t* draft_tok, int32_t gamma, float* p_logits, void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if ((st = check_gamma(e, gamma, 1.0f)) != SD_OK) return st;
+    if (!last_tok || !draft_tok || !p_logits) return fail(SD_E_INVAL, "NULL buffer");
+    forward(e, false, B, slots, last_tok, 1, draft_tok, gamma, gamma + 1, 0, p_logits, e->c.vocab,
+            (hipStream_t)stream);
+    return launched("sd_verify");
+}
+
+extern "C" sd_status sd_accept(sd_engine e, int32_t B, const int32_t* slots, const int32_t* draft_tok,
+                               const float* q_logits, const float* q_stats, const float* p_logits, int32_t gamma,
+                               float T, sd_rng rng, int32_t* out_tok, int32_t* n_emit, int32_t* next_tok,
+                               void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if ((st = check_gamma(e, gamma, T)) != SD_OK) return st;
+    if (!draft_tok || !q_logits || !q_stats || !p_logits || !out_tok || !n_emit)
+        return fail(SD_E_INVAL, "NULL buffer");
+    rows_t r = {B, 1, 0, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
+    rng_t rg = {rng.seed, rng.step};
+    launch_accept(r, gamma, e->c.vocab, T, rg, draft_tok, q_logits, q_stats, p_logits, out_tok, n_emit, next_tok,
+                  e->samp_part, e->acc_work, (hipStream_t)stream);
+    return launched("sd_accept");
+}
+
+extern "C" sd_status kv_rollback(sd_engine e, int32_t B, const int32_t* slots, const int32_t* n_emit, void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if (!n_emit) return fail(SD_E_INVAL, "n_emit is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    launch_kv_advance(B, slots, n_emit, 0, e->kv_len, e->max_slots, e->err, s);
+    if (e->poison) {
+        cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, e->c.n_kv, e->c.head_dim};
+        launch_kv_poison(B, slots, e->kv_len, e->max_gamma + 1, kv, e->c.n_layers, e->max_slots, e->max_ctx, s);
+    }
+    return launched("kv_rollback");
+}
+
+extern "C" sd_status sd_ar_step(sd_engine e, int32_t B, const int32_t* slots, const int32_t* last_tok, float T,
+                                sd_rng rng, int32_t* out_tok, float* p_logits, void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if (!(T > 0.f) || !isfinite(T)) return fail(SD_E_INVAL, "temperature must be finite and > 0");
+    if (!last_tok || !out_tok || !p_logits) return fail(SD_E_INVAL, "NULL buffer");
+    hipStream_t s = (hipStream_t)stream;
+    forward(e, false, B, slots, last_tok, 1, last_tok, 1, 1, 0, p_logits, e->c.vocab, s);
+    rows_t r = {B, 1, 0, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
+    rng_t rg = {rng.seed, rng.step};
+    launch_sample(r, p_logits, e->c.vocab, e->c.vocab, T, rg, 1, out_tok, 1, nullptr, 0, e->samp_part, s);
+    launch_kv_advance(B, slots, nullptr, 1, e->kv_len, e->max_slots, e->err, s);
+    return launched("sd_ar_step");
+}
+
+extern "C" sd_status sd_sync(sd_engine e, void* stream)
+{
+    if (!e) return fail(SD_E_INVAL, "engine is NULL");
+    HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
+    uint32_t flags[ERR_COUNT];
+    HIP_TRY(hipMemcpy(flags, e->err, sizeof flags, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemset(e->err, 0, sizeof flags));
+    if (flags[ERR_SLOT]) return fail(SD_E_INVAL, "device: slot index outside [0, max_slots)");
+    if (flags[ERR_TOKEN]) return fail(SD_E_INVAL, "device: token id outside [0, vocab)");
+    if (flags[ERR_CTX]) return fail(SD_E_INVAL, "device: position at or beyond max_ctx");
+    return SD_OK;
+}

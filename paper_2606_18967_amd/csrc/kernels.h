@@ -1,0 +1,76 @@
+// kernels.h -- launcher prototypes shared by the engine and the kernel files.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Activation element types fed to the GEMMs.
+enum act_t : int { ACT_F32 = 0, ACT_BF16 = 1, ACT_F16 = 2 };
+
+inline size_t act_bytes(act_t a) { return a == ACT_F32 ? 4 : 2; }
+
+// Row geometry of one forward call: B sequences with n new tokens each; row
+// r = b*n + i sits at absolute position kv_len[slots[b]] + off + i.
+struct rows_t {
+    int B, n, off;
+    const int32_t* slots;   // device [B]
+    const int32_t* kv_len;  // device [max_slots]
+    int max_slots, max_ctx;
+    uint32_t* err;          // device error words
+};
+
+// Cache geometry: k/v are [L][max_slots][n_kv][max_ctx][head_dim].
+struct cache_t {
+    void* k;
+    void* v;
+    int kv_f32;             // 1: fp32 cache, 0: bf16 cache
+    int n_kv, head_dim;
+};
+
+// ---- model kernels (kernels_model.hip)
+void launch_embed(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB,
+                  const void* E, int e_f32, int H, int V, float* h, hipStream_t s);
+void launch_rmsnorm(const float* h, int R, int H, const void* gain, int g_f32, float eps,
+                    void* out, act_t out_t, hipStream_t s);
+void launch_rope_kv(const rows_t& r, const float* qkv, const float2* rope, int n_q,
+                    const cache_t& c, int layer, float* q_out, hipStream_t s);
+void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer,
+                      float* part, int max_chunks, void* out, act_t out_t, hipStream_t s);
+size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks);
+int attention_chunk();
+void launch_silu_mul(const float* gu, int R, int F, void* out, act_t out_t, hipStream_t s);
+void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const,
+                       int32_t* kv_len, int max_slots, uint32_t* err, hipStream_t s);
+void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int span,
+                      const cache_t& c, int n_layers, int max_slots, int max_ctx, hipStream_t s);
+
+// ---- GEMMs (kernels_gemm.hip): C[M][N] (fp32, row stride ldc) = or += A[M][K] W^T
+enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
+void launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N, int K, int ldc,
+                      gemm_mode mode, hipStream_t s);
+void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
+                     gemm_mode mode, hipStream_t s);
+void launch_gemm_q4_f16(const _Float16* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,
+                        int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,
+                        int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+
+// ---- RTN quantizer (kernels_quant.hip)
+void launch_quant_rtn4(const void* W, int w_f32, int N, int K, uint32_t* Wq, uint16_t* Sc,
+                       hipStream_t s);
+
+// ---- sampling and acceptance (kernels_sample.hip)
+struct rng_t { uint64_t seed, step; };
+enum { STREAM_TOKEN = 0, STREAM_ACCEPT = 1, STREAM_RESIDUAL = 2 };
+int sample_chunks(int V);
+size_t sample_part_floats(int rows, int V);
+// Draws one token per row b of logits (row stride ld) with the TOKEN stream at
+// position kv_len[slots[b]] + pos_off.  Writes tok[b*tok_stride] and, if
+// stats != null, stats[b*stats_stride + {0,1}] = (max, lse) of logits/T.
+void launch_sample(const rows_t& r, const float* logits, long ld, int V, float T, rng_t rng,
+                   int pos_off, int32_t* tok, int tok_stride, float* stats, int stats_stride,
+                   float* part, hipStream_t s);
+void launch_accept(const rows_t& r, int gamma, int V, float T, rng_t rng, const int32_t* draft,
+                   const float* q_logits, const float* q_stats, const float* p_logits,
+                   int32_t* out_tok, int32_t* n_emit, int32_t* next_tok, float* part,
+                   float* work, hipStream_t s);
+size_t accept_work_floats(int B, int gamma);

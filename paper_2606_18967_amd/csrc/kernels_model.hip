@@ -1,0 +1,387 @@
+// kernels_model.hip -- decoder glue kernels: embedding gather, RMSNorm,
+// RoPE + KV-cache write, decode attention, SwiGLU, KV length bookkeeping.
+//
+// Row convention of every forward call: row r = b*n + i is token i of
+// sequence b, at absolute position kv_len[slots[b]] + off + i.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+__device__ __forceinline__ bool row_geom(const rows_t& r, int row, int* b, int* i, int* slot, int* pos)
+{
+    *b = row / r.n;
+    *i = row - *b * r.n;
+    *slot = r.slots[*b];
+    if (*slot < 0 || *slot >= r.max_slots) return false;
+    *pos = r.kv_len[*slot] + r.off + *i;
+    return *pos >= 0 && *pos < r.max_ctx;
+}
+
+template <typename T>
+__device__ __forceinline__ void store_act(void* out, size_t idx, float v);
+template <> __device__ __forceinline__ void store_act<float>(void* out, size_t idx, float v) { ((float*)out)[idx] = v; }
+template <> __device__ __forceinline__ void store_act<uint16_t>(void* out, size_t idx, float v) { ((uint16_t*)out)[idx] = f32_to_bf16(v); }
+template <> __device__ __forceinline__ void store_act<_Float16>(void* out, size_t idx, float v) { ((_Float16*)out)[idx] = (_Float16)v; }
+
+// ------------------------------------------------------------------ embed
+template <typename T>
+__global__ void __launch_bounds__(256) k_embed(rows_t r, const int32_t* tokA, int sA, const int32_t* tokB,
+                                               int sB, const T* E, int H, int V, float* h)
+{
+    int row = blockIdx.x;
+    int b = row / r.n, i = row - b * r.n;
+    int tok = (i == 0) ? tokA[(size_t)b * sA] : tokB[(size_t)b * sB + i - 1];
+    float* hr = h + (size_t)row * H;
+    if (tok < 0 || tok >= V) {
+        if (threadIdx.x == 0) flag_error(r.err, ERR_TOKEN);
+        for (int k = threadIdx.x; k < H; k += blockDim.x) hr[k] = 0.f;
+        return;
+    }
+    const T* er = E + (size_t)tok * H;
+    for (int k = threadIdx.x; k < H; k += blockDim.x) hr[k] = elem<T>::load(er, k);
+}
+
+// ------------------------------------------------------------------ rmsnorm
+template <typename G, typename O>
+__global__ void __launch_bounds__(256) k_rmsnorm(const float* h, int H, const G* gain, float eps, void* out)
+{
+    __shared__ float red[16];
+    const float* hr = h + (size_t)blockIdx.x * H;
+    float ss = 0.f;
+    for (int k = threadIdx.x; k < H; k += blockDim.x) { float v = hr[k]; ss += v * v; }
+    ss = block_sum(ss, red);
+    float inv = rsqrtf(ss / (float)H + eps);
+    for (int k = threadIdx.x; k < H; k += blockDim.x)
+        store_act<O>(out, (size_t)blockIdx.x * H + k, hr[k] * inv * elem<G>::load(gain, k));
+}
+
+// ------------------------------------------------------------------ rope + kv write
+// qkv row = [q (n_q*d) | k (n_kv*d) | v (n_kv*d)], fp32.  RoPE rotate-half with
+// the (cos, sin) table rope[pos][d/2].  q_out gets the rotated queries (fp32);
+// the rotated keys and the values go to the cache at the row's position.
+template <typename T>
+__global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, const float2* rope, int n_q,
+                                                 int n_kv, int d, T* kc, T* vc, int layer, float* q_out)
+{
+    int row = blockIdx.x;
+    int b, i, slot, pos;
+    bool ok = row_geom(r, row, &b, &i, &slot, &pos);
+    int hd = d / 2;
+    const float* src = qkv + (size_t)row * (n_q + 2 * n_kv) * d;
+    float* qo = q_out + (size_t)row * n_q * d;
+    if (!ok) {
+        if (threadIdx.x == 0) {
+            bool bad_slot = slot < 0 || slot >= r.max_slots;
+            flag_error(r.err, bad_slot ? ERR_SLOT : ERR_CTX);
+        }
+        for (int t = threadIdx.x; t < n_q * d; t += blockDim.x) qo[t] = 0.f;
+        return;
+    }
+    const float2* rp = rope + (size_t)pos * hd;
+    for (int t = threadIdx.x; t < n_q * hd; t += blockDim.x) {
+        int h = t / hd, k = t - h * hd;
+        float a = src[h * d + k], c = src[h * d + k + hd];
+        float2 cs = rp[k];
+        qo[h * d + k] = a * cs.x - c * cs.y;
+        qo[h * d + k + hd] = a * cs.y + c * cs.x;
+    }
+    const float* ks = src + n_q * d;
+    const float* vs = ks + n_kv * d;
+    size_t base = (((size_t)layer * r.max_slots + slot) * n_kv) * (size_t)r.max_ctx;
+    for (int t = threadIdx.x; t < n_kv * hd; t += blockDim.x) {
+        int h = t / hd, k = t - h * hd;
+        float a = ks[h * d + k], c = ks[h * d + k + hd];
+        float2 cs = rp[k];
+        size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
+        elem<T>::store(kc, o + k, a * cs.x - c * cs.y);
+        elem<T>::store(kc, o + k + hd, a * cs.y + c * cs.x);
+    }
+    for (int t = threadIdx.x; t < n_kv * d; t += blockDim.x) {
+        int h = t / d, k = t - h * d;
+        size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
+        elem<T>::store(vc, o + k, vs[t]);
+    }
+}
+
+// ------------------------------------------------------------------ attention
+// Split-context decode attention (flash-decoding style), fp32 arithmetic.
+// Work-group (b, kv head, chunk c) covers context positions [c*CH, (c+1)*CH)
+// of that sequence; query row (i, head h) of the sequence attends positions
+// [0, kv_len + off + i] (causal inside the block of new tokens).  Each
+// work-group writes (m, l, o[d]) per query row and head; k_attn_combine
+// merges the chunks.  D/8 lanes share one position, 8 dims per lane.
+constexpr int ATT_CH = 256;
+constexpr int ATT_RG = 4;   // query rows per pass
+
+template <typename T, int D>
+__global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, int n_q, int n_kv,
+                                                      const T* kc, const T* vc, int layer, float* part,
+                                                      int max_chunks)
+{
+    constexpr int LPP = D / 8;          // lanes per position
+    constexpr int PPW = WAVE / LPP;     // positions per wave-step
+    constexpr int NPG = 4 * PPW;        // position groups per work-group
+    __shared__ float s_m[NPG][ATT_RG];
+    __shared__ float s_l[NPG][ATT_RG];
+    __shared__ float s_o[NPG][ATT_RG][D];
+
+    int b = blockIdx.x / n_kv, kvh = blockIdx.x - b * n_kv;
+    int c = blockIdx.y;
+    int slot = r.slots[b];
+    if (slot < 0 || slot >= r.max_slots) return;   // flagged by k_rope_kv
+    int basepos = r.kv_len[slot] + r.off;
+    int ctx = basepos + r.n;
+    if (ctx > r.max_ctx) ctx = r.max_ctx;
+    int p0 = c * ATT_CH;
+    if (p0 >= ctx) return;
+    int p1 = min(p0 + ATT_CH, ctx);
+
+    int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int pg = lane / LPP;                 // position group within the wave
+    int dd = (lane % LPP) * 8;
+    int G = n_q / n_kv;
+    int QR = G * r.n;
+    float scale = rsqrtf((float)D);
+    size_t cbase = ((((size_t)layer * r.max_slots + slot) * n_kv + kvh) * (size_t)r.max_ctx) * D;
+    const T* K = kc + cbase;
+    const T* Vv = vc + cbase;
+
+    for (int rg0 = 0; rg0 < QR; rg0 += ATT_RG) {
+        float qv[ATT_RG][8], m[ATT_RG], l[ATT_RG], o[ATT_RG][8];
+        int lim[ATT_RG];
+#pragma unroll
+        for (int rr = 0; rr < ATT_RG; ++rr) {
+            int qr = rg0 + rr;
+            bool live = qr < QR;
+            int g = live ? qr / r.n : 0, i = live ? qr - g * r.n : 0;
+            int hq = kvh * G + g;
+            const float* qp = q + ((size_t)(b * r.n + i) * n_q + hq) * D + dd;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { qv[rr][e] = live ? qp[e] * scale : 0.f; o[rr][e] = 0.f; }
+            m[rr] = -INFINITY; l[rr] = 0.f;
+            lim[rr] = live ? basepos + i : -1;   // last visible position
+        }
+        for (int pb = p0 + w * PPW; pb < p1; pb += NPG) {
+            int p = pb + pg;
+            bool pv = p < p1;
+            float kf[8], vf[8];
+            if (pv) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) { kf[e] = elem<T>::load(K, (size_t)p * D + dd + e); vf[e] = elem<T>::load(Vv, (size_t)p * D + dd + e); }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) { kf[e] = 0.f; vf[e] = 0.f; }
+            }
+#pragma unroll
+            for (int rr = 0; rr < ATT_RG; ++rr) {
+                float s = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) s += qv[rr][e] * kf[e];
+#pragma unroll
+                for (int ofs = LPP / 2; ofs > 0; ofs >>= 1) s += __shfl_xor(s, ofs, WAVE);
+                if (pv && p <= lim[rr]) {
+                    float mn = fmaxf(m[rr], s);
+                    float corr = __expf(m[rr] - mn);
+                    float pe = __expf(s - mn);
+                    l[rr] = l[rr] * corr + pe;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[rr][e] = o[rr][e] * corr + pe * vf[e];
+                    m[rr] = mn;
+                }
+            }
+        }
+        // merge the NPG position groups through LDS
+        int gidx = w * PPW + pg;
+        if ((lane % LPP) == 0) {
+#pragma unroll
+            for (int rr = 0; rr < ATT_RG; ++rr) { s_m[gidx][rr] = m[rr]; s_l[gidx][rr] = l[rr]; }
+        }
+#pragma unroll
+        for (int rr = 0; rr < ATT_RG; ++rr)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s_o[gidx][rr][dd + e] = o[rr][e];
+        __syncthreads();
+        for (int t = threadIdx.x; t < ATT_RG * D; t += blockDim.x) {
+            int rr = t / D, k = t - rr * D;
+            int qr = rg0 + rr;
+            if (qr >= QR) continue;
+            float mm = -INFINITY;
+            for (int gq = 0; gq < NPG; ++gq) mm = fmaxf(mm, s_m[gq][rr]);
+            float ls = 0.f, os = 0.f;
+            if (mm > -INFINITY) {
+                for (int gq = 0; gq < NPG; ++gq) {
+                    float f = s_m[gq][rr] > -INFINITY ? __expf(s_m[gq][rr] - mm) : 0.f;
+                    ls += s_l[gq][rr] * f;
+                    os += s_o[gq][rr][k] * f;
+                }
+            }
+            int g = qr / r.n, i = qr - g * r.n;
+            int hq = kvh * G + g;
+            float* pp = part + (((size_t)(b * r.n + i) * n_q + hq) * max_chunks + c) * (D + 2);
+            if (k == 0) { pp[0] = mm; pp[1] = ls; }
+            pp[2 + k] = os;
+        }
+        __syncthreads();
+    }
+}
+
+template <typename O>
+__global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int max_chunks, void* out)
+{
+    int row = blockIdx.x / n_q, hq = blockIdx.x - row * n_q;
+    int b = row / r.n;
+    int slot = r.slots[b];
+    int ctx = 0;
+    if (slot >= 0 && slot < r.max_slots) ctx = min(r.kv_len[slot] + r.off + r.n, r.max_ctx);
+    int nch = (ctx + ATT_CH - 1) / ATT_CH;
+    if (nch > max_chunks) nch = max_chunks;
+    const float* pp = part + ((size_t)row * n_q + hq) * max_chunks * (D + 2);
+    for (int k = threadIdx.x; k < D; k += blockDim.x) {
+        float mm = -INFINITY;
+        for (int c = 0; c < nch; ++c) if (pp[c * (D + 2) + 1] > 0.f) mm = fmaxf(mm, pp[c * (D + 2)]);
+        float ls = 0.f, os = 0.f;
+        for (int c = 0; c < nch; ++c) {
+            const float* pc = pp + c * (D + 2);
+            if (pc[1] > 0.f) { float f = __expf(pc[0] - mm); ls += pc[1] * f; os += pc[2 + k] * f; }
+        }
+        store_act<O>(out, ((size_t)row * n_q + hq) * D + k, ls > 0.f ? os / ls : 0.f);
+    }
+}
+
+// ------------------------------------------------------------------ swiglu
+template <typename O>
+__global__ void __launch_bounds__(256) k_silu_mul(const float* gu, int F, void* out)
+{
+    const float* g = gu + (size_t)blockIdx.x * 2 * F;
+    const float* u = g + F;
+    for (int k = threadIdx.x; k < F; k += blockDim.x) {
+        float x = g[k];
+        store_act<O>(out, (size_t)blockIdx.x * F + k, x / (1.f + __expf(-x)) * u[k]);
+    }
+}
+
+// ------------------------------------------------------------------ kv length
+__global__ void k_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const,
+                             int32_t* kv_len, int max_slots, uint32_t* err)
+{
+    int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    int s = slots[b];
+    if (s < 0 || s >= max_slots) { flag_error(err, ERR_SLOT); return; }
+    kv_len[s] += inc ? inc[b] : inc_const;
+}
+
+template <typename T>
+__global__ void k_kv_poison(const int32_t* slots, const int32_t* kv_len, int span, T* kc, T* vc,
+                            int n_layers, int n_kv, int D, int max_slots, int max_ctx)
+{
+    int b = blockIdx.x;
+    int s = slots[b];
+    if (s < 0 || s >= max_slots) return;
+    int p0 = kv_len[s];
+    int p1 = min(p0 + span, max_ctx);
+    if (p0 < 0) p0 = 0;
+    int per = (p1 > p0 ? p1 - p0 : 0) * D;
+    size_t total = (size_t)n_layers * n_kv * per;
+    for (size_t t = threadIdx.x; t < total; t += blockDim.x) {
+        size_t lh = t / per;
+        int rem = (int)(t - lh * per);
+        int l = (int)(lh / n_kv), h = (int)(lh - (size_t)l * n_kv);
+        size_t o = ((((size_t)l * max_slots + s) * n_kv + h) * max_ctx + p0) * D + rem;
+        elem<T>::store(kc, o, __int_as_float(0x7fc00000));
+        elem<T>::store(vc, o, __int_as_float(0x7fc00000));
+    }
+}
+
+}  // namespace
+
+// ======================================================================= launchers
+void launch_embed(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB,
+                  const void* E, int e_f32, int H, int V, float* h, hipStream_t s)
+{
+    int R = r.B * r.n;
+    if (e_f32) k_embed<float><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, (const float*)E, H, V, h);
+    else k_embed<uint16_t><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, (const uint16_t*)E, H, V, h);
+}
+
+template <typename G>
+static void rmsnorm_t(const float* h, int R, int H, const G* g, float eps, void* out, act_t t, hipStream_t s)
+{
+    if (t == ACT_F32) k_rmsnorm<G, float><<<R, 256, 0, s>>>(h, H, g, eps, out);
+    else if (t == ACT_BF16) k_rmsnorm<G, uint16_t><<<R, 256, 0, s>>>(h, H, g, eps, out);
+    else k_rmsnorm<G, _Float16><<<R, 256, 0, s>>>(h, H, g, eps, out);
+}
+
+void launch_rmsnorm(const float* h, int R, int H, const void* gain, int g_f32, float eps, void* out,
+                    act_t out_t, hipStream_t s)
+{
+    if (g_f32) rmsnorm_t(h, R, H, (const float*)gain, eps, out, out_t, s);
+    else rmsnorm_t(h, R, H, (const uint16_t*)gain, eps, out, out_t, s);
+}
+
+void launch_rope_kv(const rows_t& r, const float* qkv, const float2* rope, int n_q, const cache_t& c,
+                    int layer, float* q_out, hipStream_t s)
+{
+    int R = r.B * r.n;
+    if (c.kv_f32)
+        k_rope_kv<float><<<R, 256, 0, s>>>(r, qkv, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v, layer, q_out);
+    else
+        k_rope_kv<uint16_t><<<R, 256, 0, s>>>(r, qkv, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
+                                              (uint16_t*)c.v, layer, q_out);
+}
+
+int attention_chunk() { return ATT_CH; }
+
+size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
+{
+    return (size_t)R * n_q * max_chunks * (head_dim + 2);
+}
+
+template <typename T, int D>
+static void attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
+                   int max_chunks, void* out, act_t out_t, hipStream_t s)
+{
+    dim3 grid(r.B * c.n_kv, max_chunks);
+    k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
+    int R = r.B * r.n;
+    if (out_t == ACT_F32) k_attn_combine<float><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
+    else if (out_t == ACT_BF16) k_attn_combine<uint16_t><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
+    else k_attn_combine<_Float16><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
+}
+
+void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
+                      int max_chunks, void* out, act_t out_t, hipStream_t s)
+{
+    if (c.head_dim == 128) {
+        if (c.kv_f32) attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+        else attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+    } else {
+        if (c.kv_f32) attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+        else attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+    }
+}
+
+void launch_silu_mul(const float* gu, int R, int F, void* out, act_t out_t, hipStream_t s)
+{
+    if (out_t == ACT_F32) k_silu_mul<float><<<R, 256, 0, s>>>(gu, F, out);
+    else if (out_t == ACT_BF16) k_silu_mul<uint16_t><<<R, 256, 0, s>>>(gu, F, out);
+    else k_silu_mul<_Float16><<<R, 256, 0, s>>>(gu, F, out);
+}
+
+void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const, int32_t* kv_len,
+                       int max_slots, uint32_t* err, hipStream_t s)
+{
+    k_kv_advance<<<(B + 255) / 256, 256, 0, s>>>(B, slots, inc, inc_const, kv_len, max_slots, err);
+}
+
+void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int span, const cache_t& c,
+                      int n_layers, int max_slots, int max_ctx, hipStream_t s)
+{
+    if (c.kv_f32)
+        k_kv_poison<float><<<B, 256, 0, s>>>(slots, kv_len, span, (float*)c.k, (float*)c.v, n_layers, c.n_kv,
+                                             c.head_dim, max_slots, max_ctx);
+    else
+        k_kv_poison<uint16_t><<<B, 256, 0, s>>>(slots, kv_len, span, (uint16_t*)c.k, (uint16_t*)c.v, n_layers,
+                                                c.n_kv, c.head_dim, max_slots, max_ctx);
+}

@@ -1,0 +1,139 @@
+"""GPU parity of single SD stages through the C ABI:
+  - the drafter refresh (RTN int4 codes and fp16 scales bit-exact with the
+    oracle, unpacked from the documented tile layout);
+  - speculative rejection sampling on identical logits (decisions identical
+    to the oracle's except at documented near-ties), for one and for many
+    vocabulary chunks;
+  - device range errors are reported by sd_sync without touching memory out
+    of bounds."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.parity import drafter_layout, unpack_q4
+from paper_2606_18967_amd import sdrl, synth
+
+from gpu_common import host_bits, i32, make_engine, say
+
+pytestmark = pytest.mark.gpu
+
+SMALL_BF16 = dict(name="small-bf16", n_layers=2, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=512, vocab=256,
+                  dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY, SMALL_BF16], ids=["tiny-f32", "small-bf16"])
+def test_refresh_drafter_bit_exact(cfg):
+    say("refresh_drafter", cfg["name"])
+    W = synth.make_weights(cfg, 5, "cpu")
+    # edge groups: all zero, huge magnitude, tiny magnitude
+    W[4][3, 128:256] = 0
+    W[4][5, :128] *= 1000
+    W[8][1, 0:128] *= 1e-4
+    Wd = [w.cuda() for w in W]
+    eng, *_ = make_engine(cfg, Wd, 1, 8, 1)
+    qbuf = eng.refresh_drafter()
+    torch.cuda.synchronize()
+    host = qbuf.cpu().numpy()
+    Wh = host_bits(W)
+    kind = oracle.BF16 if cfg["dtype"] == "bf16" else oracle.F32
+    layout, total = drafter_layout(cfg)
+    assert total == host.size
+    widx = [1, 2, 4, 5]
+    for l, w, N, K, co, so in layout:
+        codes, sc = unpack_q4(host[co:co + N * K // 2], host[so:so + N * (K // 128) * 2], N, K)
+        want_c, want_s = oracle.quantize_rtn4(oracle.tensor_f32(Wh[3 + 6 * l + widx[w]], kind))
+        assert np.array_equal(codes, want_c), (l, w)
+        assert np.array_equal(sc, want_s), (l, w)
+    eng.close()
+
+
+def _accept_case(V, B, gamma, mode, seed):
+    rng = np.random.default_rng(seed)
+    q = (rng.standard_normal((B, gamma, V)) * 2).astype(np.float32)
+    if mode == "close":
+        p = np.concatenate([q, q[:, -1:]], 1) + rng.standard_normal((B, gamma + 1, V)).astype(np.float32) * 0.3
+    else:
+        p = (rng.standard_normal((B, gamma + 1, V)) * 2).astype(np.float32)
+    return q, p.astype(np.float32)
+
+
+@pytest.mark.parametrize("V,mode", [(1024, "close"), (1024, "indep"), (128256, "close"), (128256, "indep")])
+def test_accept_matches_oracle_on_identical_logits(V, mode):
+    say("accept", V, mode)
+    B, gamma, T, seed, step = 16, 4, 1.0, 21, 5
+    cfg = dict(name="acc", n_layers=1, hidden=128, n_q=2, n_kv=1, head_dim=64, ffn=128, vocab=V, dtype="f32",
+               rope_theta=10000.0, rms_eps=1e-5)
+    W = [w.cuda() for w in synth.make_weights(cfg, 1, "cpu")]
+    eng, k, v, kv_len = make_engine(cfg, W, B, 1024, gamma)
+    rng = np.random.default_rng(V)
+    lens = rng.integers(0, 900, B).astype(np.int32)
+    kv_len.copy_(i32(lens))
+    slots = np.arange(B, dtype=np.int32)[::-1].copy()       # slot order differs from row order
+    q, p = _accept_case(V, B, gamma, mode, V + len(mode))
+    draft = np.zeros((B, gamma), np.int32)
+    qstats = np.zeros((B, gamma, 2), np.float32)
+    for b in range(B):
+        s = int(slots[b])
+        for j in range(gamma):
+            draft[b, j], _ = oracle.sample_row(q[b, j], T, seed, step, oracle.STREAM_TOKEN, s, int(lens[s]) + j + 1)
+            qstats[b, j] = oracle.row_stats(q[b, j], T)
+    out = torch.zeros((B, gamma + 1), dtype=torch.int32, device="cuda")
+    n_emit = torch.zeros(B, dtype=torch.int32, device="cuda")
+    nxt = torch.zeros(B, dtype=torch.int32, device="cuda")
+    eng.accept(i32(slots), i32(draft), torch.tensor(q, device="cuda"), torch.tensor(qstats, device="cuda"),
+               torch.tensor(p, device="cuda"), gamma, T, seed, step, out, n_emit, nxt)
+    eng.sync()
+    out, n_emit, nxt = out.cpu().numpy(), n_emit.cpu().numpy(), nxt.cpu().numpy()
+    exempt, rejections = 0, 0
+    for b in range(B):
+        s = int(slots[b])
+        n, o, ratio, u, gap = oracle.accept_seq(draft[b], q[b], p[b], T, seed, step, s, int(lens[s]))
+        rejections += n <= gamma
+        if n == n_emit[b] and np.array_equal(o[:n], out[b, :n]):
+            assert nxt[b] == o[n - 1]
+            assert np.all(out[b, n:] == -1)
+            continue
+        k_ = min(n, int(n_emit[b]))
+        near = k_ <= gamma and abs(u[k_ - 1] - ratio[k_ - 1]) < 1e-3
+        near = near or (n == n_emit[b] and gap < 1e-4 * 20)
+        assert near, (b, n, o, n_emit[b], out[b], u, ratio, gap)
+        exempt += 1
+    assert exempt <= 2
+    if mode == "indep":
+        assert rejections >= B // 2
+    eng.close()
+
+
+def test_device_range_errors_are_reported():
+    say("range errors")
+    cfg = synth.TINY
+    W = [w.cuda() for w in synth.make_weights(cfg, 2, "cpu")]
+    B, gamma = 4, 2
+    eng, k, v, kv_len = make_engine(cfg, W, B, 64, gamma)
+    bufs = sdrl.SDBuffers(eng, B, gamma)
+    last = i32([1, 2, 3, 4])
+    # a slot index beyond max_slots
+    sdrl.sd_step(eng, bufs, i32([0, 1, 2, 7]), last, 1.0, 0, 0)
+    with pytest.raises(sdrl.SDError, match="slot"):
+        eng.sync()
+    # a token id beyond the vocabulary
+    eng.ar_step(i32([0]), i32([9999]), 1.0, 0, 0, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                torch.zeros((1, cfg["vocab"]), dtype=torch.float32, device="cuda"))
+    with pytest.raises(sdrl.SDError, match="token"):
+        eng.sync()
+    # positions past max_ctx
+    kv_len.fill_(62)
+    sdrl.sd_step(eng, bufs, i32([0, 1, 2, 3]), last, 1.0, 0, 0)
+    with pytest.raises(sdrl.SDError, match="max_ctx"):
+        eng.sync()
+    # host-side argument checks
+    with pytest.raises(sdrl.SDError):
+        eng.draft(i32([0]), i32([1]), 5, 1.0, 0, 0, torch.zeros((1, 5), dtype=torch.int32, device="cuda"),
+                  torch.zeros((1, 5, cfg["vocab"]), device="cuda"), torch.zeros((1, 5, 2), device="cuda"))
+    with pytest.raises(ValueError):
+        eng.verify(i32([0]), i32([1]), torch.zeros((1, 2), dtype=torch.int32, device="cuda"), 2,
+                   torch.zeros((1, 2, cfg["vocab"]), device="cuda"))
+    kv_len.zero_()
+    eng.sync()
+    eng.close()
