@@ -186,6 +186,18 @@ sd_status sd_sync(sd_engine e, void* stream);
 /* Debug switch: 1 = kv_rollback poisons discarded KV with NaN. */
 sd_status sd_set_debug(sd_engine e, int32_t poison);
 
+/* Kernel timing (diagnostics).  While on, the engine brackets each launch of
+ * a kernel class with HIP events recorded on the launch stream.  Classes:
+ * 0 attention, 1 int4 projections (drafter), 2 bf16/fp32 projections
+ * (target layers), 3 LM head, 4 token sampler, 5 accept, 6 norms / RoPE /
+ * embedding / SwiGLU / KV bookkeeping.  sd_timing(e, 1) also clears the
+ * accumulated records. */
+sd_status sd_timing(sd_engine e, int32_t on);
+
+/* Waits for the recorded events and returns, for class `cls`, the summed
+ * kernel time in milliseconds and the number of launches (host pointers). */
+sd_status sd_timing_read(sd_engine e, int32_t cls, double* total_ms, int32_t* launches);
+
 /* ------------------------------------------------ host policy (no GPU) */
 
 /* Roofline cost model of Sec. 4.2 / App. D.2.  Architecture terms: W_T, W_D

@@ -45,6 +45,7 @@ static sd_status launched(const char* what)
 
 // ------------------------------------------------------------------ engine
 enum { PRJ_QKV = 0, PRJ_O = 1, PRJ_GU = 2, PRJ_DOWN = 3 };
+enum { T_ATTN = 0, T_Q4 = 1, T_PROJ = 2, T_LMHEAD = 3, T_SAMPLE = 4, T_ACCEPT = 5, T_MISC = 6, T_CLASSES = 7 };
 
 struct sd_engine_s {
     sd_model_cfg c;
@@ -74,6 +75,43 @@ struct sd_engine_s {
     float* acc_work = nullptr;
     float2* rope = nullptr;
     uint32_t* err = nullptr;
+    float* gpart = nullptr;      // split-K partial sums
+    size_t gpart_cap = 0;        // floats
+    // kernel timing (diagnostics)
+    bool timing = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_used = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> marks[T_CLASSES];
+};
+
+// Brackets the launches made during its lifetime with events of class cls.
+struct tscope {
+    sd_engine e;
+    int cls;
+    hipStream_t s;
+    hipEvent_t stop = nullptr;
+    tscope(sd_engine e_, int cls_, hipStream_t s_) : e(e_), cls(cls_), s(s_)
+    {
+        if (!e->timing) return;
+        hipEvent_t start = next_event(e);
+        stop = next_event(e);
+        if (!start || !stop) { stop = nullptr; return; }
+        (void)hipEventRecord(start, s);
+        e->marks[cls].push_back({start, stop});
+    }
+    ~tscope()
+    {
+        if (stop) (void)hipEventRecord(stop, s);
+    }
+    static hipEvent_t next_event(sd_engine e)
+    {
+        if (e->ev_used == e->ev_pool.size()) {
+            hipEvent_t ev;
+            if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+            e->ev_pool.push_back(ev);
+        }
+        return e->ev_pool[e->ev_used++];
+    }
 };
 
 static void prj_shape(const sd_model_cfg& c, int which, int* N, int* K)
@@ -132,9 +170,30 @@ extern "C" size_t sd_drafter_bytes(const sd_model_cfg* c)
     return total * (size_t)c->n_layers;
 }
 
+// Largest split-K scratch any projection or the LM head needs for up to R rows.
+static size_t gpart_bytes(const sd_model_cfg& c, int R)
+{
+    if (c.dtype == SD_DTYPE_F32) return 256;
+    size_t mx = 0;
+    for (int M = 1; M <= R; M = (M < 64 ? M + 1 : M + 64)) {
+        int m = M > R ? R : M;
+        for (int w = 0; w < 4; ++w) {
+            int N, K;
+            prj_shape(c, w, &N, &K);
+            size_t f = gemm_part_floats(m, N, K);
+            mx = f > mx ? f : mx;
+        }
+        size_t f = gemm_part_floats(m, c.vocab, c.hidden);
+        mx = f > mx ? f : mx;
+    }
+    { int m = R; for (int w = 0; w < 4; ++w) { int N, K; prj_shape(c, w, &N, &K); size_t f = gemm_part_floats(m, N, K); mx = f > mx ? f : mx; } }
+    return (mx > 64 ? mx : 64) * 4;
+}
+
 static void free_ws(sd_engine e)
 {
-    void* ps[] = {e->h, e->a, e->qkv, e->qrot, e->att, e->gu, e->act, e->att_part, e->samp_part, e->acc_work, e->rope, e->err};
+    void* ps[] = {e->h, e->a, e->qkv, e->qrot, e->att, e->gu, e->act, e->att_part, e->samp_part, e->acc_work, e->rope, e->err,
+                  e->gpart};
     for (void* p : ps)
         if (p) (void)hipFree(p);
 }
@@ -176,7 +235,9 @@ extern "C" sd_status sd_create(const sd_model_cfg* cfg, int32_t max_slots, int32
         {(void**)&e->acc_work, accept_work_floats(max_slots, max_gamma) * 4},
         {(void**)&e->rope, (size_t)max_ctx * (c.head_dim / 2) * sizeof(float2)},
         {(void**)&e->err, ERR_COUNT * 4},
+        {(void**)&e->gpart, gpart_bytes(c, e->rows_max)},
     };
+    e->gpart_cap = gpart_bytes(c, e->rows_max) / 4;
     for (auto& al : allocs) {
         if (hipMalloc(al.p, al.bytes) != hipSuccess) {
             free_ws(e);
@@ -208,6 +269,7 @@ extern "C" sd_status sd_destroy(sd_engine e)
     if (!e) return fail(SD_E_INVAL, "engine is NULL");
     (void)hipDeviceSynchronize();
     free_ws(e);
+    for (hipEvent_t ev : e->ev_pool) (void)hipEventDestroy(ev);
     delete e;
     return SD_OK;
 }
@@ -281,11 +343,11 @@ static void proj(sd_engine e, bool draft, int layer, int which, const void* A, f
         const uint32_t* q = e->qw[4 * layer + which];
         const uint16_t* sc = e->qs[4 * layer + which];
         if (e->f32) launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s);
-        else launch_gemm_q4_f16((const _Float16*)A, q, sc, C, M, N, K, ldc, mode, s);
+        else launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
     } else {
         const void* w = W(e, layer, widx[which]);
         if (e->f32) launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s);
-        else launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, M, N, K, ldc, mode, s);
+        else launch_gemm_stream(1, (const uint16_t*)A, w, nullptr, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
     }
 }
 
@@ -301,24 +363,27 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
     int R = B * n;
     act_t at = act_of(e, draft);
     int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
-    launch_embed(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, s);
+    int pcls = draft ? T_Q4 : T_PROJ;
+    { tscope t(e, T_MISC, s); launch_embed(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, s); }
     for (int l = 0; l < c.n_layers; ++l) {
-        launch_rmsnorm(e->h, R, c.hidden, W(e, l, 0), e->f32, c.rms_eps, e->a, at, s);
-        proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s);
-        launch_rope_kv(r, e->qkv, e->rope, c.n_q, kv, l, e->qrot, s);
-        launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s);
-        proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s);
-        launch_rmsnorm(e->h, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s);
-        proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s);
-        launch_silu_mul(e->gu, R, c.ffn, e->act, at, s);
-        proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s);
+        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, W(e, l, 0), e->f32, c.rms_eps, e->a, at, s); }
+        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s); }
+        { tscope t(e, T_MISC, s); launch_rope_kv(r, e->qkv, e->rope, c.n_q, kv, l, e->qrot, s); }
+        { tscope t(e, T_ATTN, s); launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s); }
+        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
+        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }
+        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s); }
+        { tscope t(e, T_MISC, s); launch_silu_mul(e->gu, R, c.ffn, e->act, at, s); }
+        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s); }
     }
     if (logits) {
         // the LM head stays in the target precision for the drafter too
         act_t lt = e->f32 ? ACT_F32 : ACT_BF16;
-        launch_rmsnorm(e->h, R, c.hidden, e->w[1], e->f32, c.rms_eps, e->a, lt, s);
+        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, e->w[1], e->f32, c.rms_eps, e->a, lt, s); }
+        tscope t(e, T_LMHEAD, s);
         if (e->f32) launch_gemm_f32((const float*)e->a, (const float*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
-        else launch_gemm_bf16((const uint16_t*)e->a, (const uint16_t*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
+        else launch_gemm_stream(1, (const uint16_t*)e->a, e->w[2], nullptr, logits, e->gpart, e->gpart_cap, R, c.vocab,
+                                c.hidden, (int)ldl, GEMM_STORE, s);
     }
 }
 
@@ -374,6 +439,7 @@ extern "C" sd_status sd_draft(sd_engine e, int32_t B, const int32_t* slots, cons
         int stride = j == 1 ? 1 : gamma;
         float* lg = q_logits + (size_t)(j - 1) * V;
         forward(e, true, B, slots, tok, stride, tok, stride, 1, j - 1, lg, ld, s);
+        tscope t(e, T_SAMPLE, s);
         launch_sample(r, lg, ld, V, T, rg, j, draft_tok + (j - 1), gamma, q_stats + 2 * (j - 1), 2 * gamma,
                       e->samp_part, s);
     }
@@ -404,6 +470,7 @@ extern "C" sd_status sd_accept(sd_engine e, int32_t B, const int32_t* slots, con
         return fail(SD_E_INVAL, "NULL buffer");
     rows_t r = {B, 1, 0, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
     rng_t rg = {rng.seed, rng.step};
+    tscope t(e, T_ACCEPT, (hipStream_t)stream);
     launch_accept(r, gamma, e->c.vocab, T, rg, draft_tok, q_logits, q_stats, p_logits, out_tok, n_emit, next_tok,
                   e->samp_part, e->acc_work, (hipStream_t)stream);
     return launched("sd_accept");
@@ -415,6 +482,7 @@ extern "C" sd_status kv_rollback(sd_engine e, int32_t B, const int32_t* slots, c
     if (st != SD_OK) return st;
     if (!n_emit) return fail(SD_E_INVAL, "n_emit is NULL");
     hipStream_t s = (hipStream_t)stream;
+    tscope t(e, T_MISC, s);
     launch_kv_advance(B, slots, n_emit, 0, e->kv_len, e->max_slots, e->err, s);
     if (e->poison) {
         cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, e->c.n_kv, e->c.head_dim};
@@ -434,8 +502,8 @@ extern "C" sd_status sd_ar_step(sd_engine e, int32_t B, const int32_t* slots, co
     forward(e, false, B, slots, last_tok, 1, last_tok, 1, 1, 0, p_logits, e->c.vocab, s);
     rows_t r = {B, 1, 0, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
     rng_t rg = {rng.seed, rng.step};
-    launch_sample(r, p_logits, e->c.vocab, e->c.vocab, T, rg, 1, out_tok, 1, nullptr, 0, e->samp_part, s);
-    launch_kv_advance(B, slots, nullptr, 1, e->kv_len, e->max_slots, e->err, s);
+    { tscope t(e, T_SAMPLE, s); launch_sample(r, p_logits, e->c.vocab, e->c.vocab, T, rg, 1, out_tok, 1, nullptr, 0, e->samp_part, s); }
+    { tscope t(e, T_MISC, s); launch_kv_advance(B, slots, nullptr, 1, e->kv_len, e->max_slots, e->err, s); }
     return launched("sd_ar_step");
 }
 
@@ -449,5 +517,33 @@ extern "C" sd_status sd_sync(sd_engine e, void* stream)
     if (flags[ERR_SLOT]) return fail(SD_E_INVAL, "device: slot index outside [0, max_slots)");
     if (flags[ERR_TOKEN]) return fail(SD_E_INVAL, "device: token id outside [0, vocab)");
     if (flags[ERR_CTX]) return fail(SD_E_INVAL, "device: position at or beyond max_ctx");
+    return SD_OK;
+}
+
+extern "C" sd_status sd_timing(sd_engine e, int32_t on)
+{
+    if (!e) return fail(SD_E_INVAL, "engine is NULL");
+    if (on) {
+        HIP_TRY(hipDeviceSynchronize());
+        for (auto& m : e->marks) m.clear();
+        e->ev_used = 0;
+    }
+    e->timing = on != 0;
+    return SD_OK;
+}
+
+extern "C" sd_status sd_timing_read(sd_engine e, int32_t cls, double* total_ms, int32_t* launches)
+{
+    if (!e || !total_ms || !launches) return fail(SD_E_INVAL, "NULL argument");
+    if (cls < 0 || cls >= T_CLASSES) return fail(SD_E_INVAL, "timing class %d outside [0, %d)", cls, (int)T_CLASSES);
+    double tot = 0.0;
+    for (auto& m : e->marks[cls]) {
+        HIP_TRY(hipEventSynchronize(m.second));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, m.first, m.second));
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = (int32_t)e->marks[cls].size();
     return SD_OK;
 }

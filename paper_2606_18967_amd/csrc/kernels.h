@@ -45,12 +45,14 @@ void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int sp
 
 // ---- GEMMs (kernels_gemm.hip): C[M][N] (fp32, row stride ldc) = or += A[M][K] W^T
 enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
-void launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N, int K, int ldc,
-                      gemm_mode mode, hipStream_t s);
+// Weight-streaming MFMA GEMM: wf 0 = int4 packed weights (Wt, scales Sc) with
+// fp16 activations, wf 1 = bf16 weights and activations.  part is split-K
+// scratch of part_cap floats (no split when too small).
+void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
+                        size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+size_t gemm_part_floats(int M, int N, int K);
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
                      gemm_mode mode, hipStream_t s);
-void launch_gemm_q4_f16(const _Float16* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,
-                        int N, int K, int ldc, gemm_mode mode, hipStream_t s);
 void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,
                         int N, int K, int ldc, gemm_mode mode, hipStream_t s);
 

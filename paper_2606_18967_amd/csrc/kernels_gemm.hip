@@ -1,11 +1,11 @@
 // kernels_gemm.hip -- the projections: C[M][N] (fp32) = or += A[M][K] W^T.
 //
 // Weights are row-major [N][K] (K contiguous), activations [M][K].
-//   - gemm_bf16:  bf16 x bf16 on MFMA (v_mfma_f32_16x16x32_bf16), LDS-tiled.
-//   - gemm_q4_f16: int4 group-128 weights in the packed tile layout written by
-//     the RTN quantizer, dequantized in registers to exact fp16 integers and
-//     fed to v_mfma_f32_16x16x32_f16; the per-group fp16 scale is applied to
-//     the fp32 partial sum of each group.
+//   - gemm_stream (bf16 or int4 weights, MFMA): see k_gemm_stream.  int4
+//     group-128 weights in the packed tile layout written by the RTN quantizer
+//     are dequantized in registers to exact fp16 integers and fed to
+//     v_mfma_f32_16x16x32_f16; the per-group fp16 scale is applied to the fp32
+//     partial sum of each group.
 //   - gemm_f32 / gemm_q4_f32: plain VALU versions for fp32 models.
 //
 // Packed int4 layout (per weight matrix, N % 16 == 0, K % 128 == 0): for
@@ -18,80 +18,6 @@
 #include "kernels.h"
 
 namespace {
-
-// ------------------------------------------------------------------ bf16 MFMA
-constexpr int BM = 64, BN = 64, BK = 64, LDT = BK + 8;   // padded LDS row (bf16 elements)
-
-__global__ void __launch_bounds__(256) k_gemm_bf16(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
-                                                   float* __restrict__ C, int M, int N, int K, int ldc, int mode)
-{
-    __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDT];
-    __shared__ __attribute__((aligned(16))) uint16_t Ws[BN * LDT];
-    int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    int wm = w >> 1, wn = w & 1;
-    int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-    floatx4 acc[2][2];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = (floatx4){0.f, 0.f, 0.f, 0.f};
-
-    for (int k0 = 0; k0 < K; k0 += BK) {
-        // 64 rows x 64 k = 512 chunks of 8 bf16 for each operand, 2 per thread
-        u32x4 ra[2], rw[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            int ch = tid + t * 256;
-            int row = ch >> 3, kc = (ch & 7) * 8;
-            int gm = m0 + row;
-            ra[t] = gm < M ? *(const u32x4*)(A + (size_t)gm * K + k0 + kc) : (u32x4){0u, 0u, 0u, 0u};
-            rw[t] = *(const u32x4*)(W + (size_t)(n0 + row) * K + k0 + kc);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            int ch = tid + t * 256;
-            int row = ch >> 3, kc = (ch & 7) * 8;
-            *(u32x4*)(As + row * LDT + kc) = ra[t];
-            *(u32x4*)(Ws + row * LDT + kc) = rw[t];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            int kk = ks * 32 + (lane >> 4) * 8;
-            bf16x8 af[2], bfr[2];
-#pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                int row = wm * 32 + a * 16 + (lane & 15);
-                af[a] = *(const bf16x8*)(As + row * LDT + kk);
-            }
-#pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                int row = wn * 32 + b * 16 + (lane & 15);
-                bfr[b] = *(const bf16x8*)(Ws + row * LDT + kk);
-            }
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
-        }
-    }
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            int col = n0 + wn * 32 + b * 16 + (lane & 15);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                int row = m0 + wm * 32 + a * 16 + (lane >> 4) * 4 + i;
-                if (row < M) {
-                    float* cp = C + (size_t)row * ldc + col;
-                    *cp = mode == GEMM_ADD ? *cp + acc[a][b][i] : acc[a][b][i];
-                }
-            }
-        }
-}
 
 // ------------------------------------------------------------------ fp32 VALU
 constexpr int FT = 64, FK = 16;
@@ -157,61 +83,177 @@ __device__ __forceinline__ half8 dequant8(uint32_t x)
 
 __device__ __forceinline__ float f16_bits_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 
-// ------------------------------------------------------------------ int4 x fp16 MFMA
-// One wave per (16-column n-block, 64-row m-tile); A fragments straight from
-// global memory.
-__global__ void __launch_bounds__(64) k_gemm_q4_f16(const _Float16* __restrict__ A, const uint32_t* __restrict__ Wq,
-                                                    const uint16_t* __restrict__ Sc, float* __restrict__ C, int M,
-                                                    int N, int K, int ldc, int mode)
+// ------------------------------------------------------------------ weight-streaming MFMA GEMM
+// C[M][N] = A[M][K] W^T for decode-shaped M (a few to a few hundred rows).
+// A work-group covers a 64-row m-tile, 64*NBW columns (NBW 16-column blocks
+// per wave, 4 waves) and a range of K split into chunks of 128.  The A chunk
+// is staged in LDS (double-buffered) and shared by the four waves; each wave
+// streams its weight columns from HBM straight into registers one chunk
+// ahead of the MFMAs, so every weight byte is read once per m-tile.  With
+// several K splits the partial sums go to P[s][M][N] and k_splitk_reduce adds
+// them up.  Work items are laid out so that consecutive ones (the m-tiles of
+// one column tile) land on the same XCD and share its L2.
+//   WF = 0: int4 packed weights, fp16 activations (v_mfma_f32_16x16x32_f16);
+//           in chunk g, k-step j, lane l covers k = 128g + 32j + 8(l/16) + 0..7.
+//   WF = 1: bf16 weights and activations (v_mfma_f32_16x16x32_bf16); lane l
+//           covers k = 128g + 32(l/16) + 8j + 0..7 so that its 64 bytes of a
+//           weight row are contiguous.
+constexpr int SK = 128;          // k per chunk (= one quantization group)
+constexpr int ALD = SK + 8;      // LDS row stride in 2-byte elements
+constexpr int SM = 64;           // rows per m-tile
+
+template <int WF, int NBW, int MT>
+__global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict__ A, const void* __restrict__ Wt,
+                                                     const uint16_t* __restrict__ Sc, float* __restrict__ C,
+                                                     float* __restrict__ P, int M, int N, int K, int ldc, int mode,
+                                                     int S, int msup, int total)
 {
-    int lane = threadIdx.x;
-    int nb = blockIdx.x;
-    int m0 = blockIdx.y * 64;
-    int G = K / 128;
-    int mtiles = min(4, (M - m0 + 15) / 16);
-    floatx4 acc[4];
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][SM * ALD];
+    const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
+    const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (w >= total) return;
+    const int ms = w % msup, rest = w / msup;
+    const int s = rest % S, tile = rest / S;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int m0 = ms * SM;
+    const int G = K / SK, Gs = G / S, g0 = s * Gs, g1 = g0 + Gs;
+    const int nb0 = (tile * 4 + wv) * NBW;
+    const int rows = min(M - m0, MT * 16);                  // rows staged (others stay zero)
+
+    // ---- loaders
+    u32x4 a_reg[4];
+    auto load_a = [&](int g) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[t] = (floatx4){0.f, 0.f, 0.f, 0.f};
-    const u32x4* wp = (const u32x4*)Wq + (size_t)nb * G * 64 + lane;
-    const uint16_t* sp = Sc + (size_t)nb * G * 16 + (lane & 15);
-    int arow = lane & 15, akc = (lane >> 4) * 8;
-    for (int g = 0; g < G; ++g) {
-        u32x4 wv = wp[(size_t)g * 64];
-        float s = f16_bits_to_f32(sp[(size_t)g * 16]);
-        floatx4 tmp[4];
+        for (int t = 0; t < 4; ++t) {
+            int pidx = tid + t * 256;
+            int row = pidx >> 4, col = (pidx & 15) * 8;
+            a_reg[t] = (row < rows) ? *(const u32x4*)(A + (size_t)(m0 + row) * K + (size_t)g * SK + col)
+                                    : (u32x4){0u, 0u, 0u, 0u};
+        }
+    };
+    auto store_a = [&](int buf) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) tmp[t] = (floatx4){0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < 4; ++t) {
+            int pidx = tid + t * 256;
+            int row = pidx >> 4, col = (pidx & 15) * 8;
+            if (row < MT * 16) *(u32x4*)(&As[buf][row * ALD + col]) = a_reg[t];
+        }
+    };
+    constexpr int WV = WF == 0 ? 1 : 4;                     // 16-byte vectors per lane per block per chunk
+    u32x4 wcur[NBW][WV], wnext[NBW][WV];
+    uint16_t scur[NBW], snext[NBW];
+    auto load_w = [&](int g, u32x4 (&wr)[NBW][WV], uint16_t (&sr)[NBW]) {
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) {
+            int nb = nb0 + i;
+            if constexpr (WF == 0) {
+                wr[i][0] = ((const u32x4*)Wt)[((size_t)nb * G + g) * 64 + lane];
+                sr[i] = Sc[((size_t)nb * G + g) * 16 + (lane & 15)];
+            } else {
+                const uint16_t* wp = (const uint16_t*)Wt + (size_t)(nb * 16 + (lane & 15)) * K + (size_t)g * SK +
+                                     32 * (lane >> 4);
+#pragma unroll
+                for (int j = 0; j < WV; ++j) wr[i][j] = *(const u32x4*)(wp + 8 * j);
+                sr[i] = 0;
+            }
+        }
+    };
+
+    floatx4 acc[NBW][MT];
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[i][t] = (floatx4){0.f, 0.f, 0.f, 0.f};
+
+    load_w(g0, wcur, scur);
+    load_a(g0);
+    store_a(0);
+    __syncthreads();
+
+    for (int g = g0; g < g1; ++g) {
+        const int buf = (g - g0) & 1;
+        const bool more = g + 1 < g1;
+        if (more) { load_w(g + 1, wnext, snext); load_a(g + 1); }
+        floatx4 tmp[NBW][MT];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            half8 bq = dequant8(wv[j]);
-            int k = g * 128 + j * 32 + akc;
+            const int acol = WF == 0 ? 32 * j + 8 * (lane >> 4) : 32 * (lane >> 4) + 8 * j;
+            uint16_t* ab = &As[buf][(lane & 15) * ALD + acol];
+            u32x4 af[MT];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                if (t < mtiles) {
-                    int row = m0 + t * 16 + arow;
-                    half8 af = row < M ? *(const half8*)(A + (size_t)row * K + k) : (half8){};
-                    tmp[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, bq, tmp[t], 0, 0, 0);
+            for (int t = 0; t < MT; ++t) af[t] = *(const u32x4*)(ab + t * 16 * ALD);
+#pragma unroll
+            for (int i = 0; i < NBW; ++i) {
+                if constexpr (WF == 0) {
+                    half8 bq = dequant8(wcur[i][0][j]);
+#pragma unroll
+                    for (int t = 0; t < MT; ++t)
+                        tmp[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            __builtin_bit_cast(half8, af[t]), bq, j == 0 ? (floatx4){0.f, 0.f, 0.f, 0.f} : tmp[i][t],
+                            0, 0, 0);
+                } else {
+                    bf16x8 bb = __builtin_bit_cast(bf16x8, wcur[i][j]);
+#pragma unroll
+                    for (int t = 0; t < MT; ++t)
+                        acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[t]), bb,
+                                                                           acc[i][t], 0, 0, 0);
                 }
             }
         }
+        if constexpr (WF == 0) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+            for (int i = 0; i < NBW; ++i) {
+                float sc = f16_bits_to_f32(scur[i]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[t][i] += s * tmp[t][i];
-    }
-    int col = nb * 16 + (lane & 15);
+                for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        if (t >= mtiles) continue;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            int row = m0 + t * 16 + (lane >> 4) * 4 + i;
-            if (row < M) {
-                float* cp = C + (size_t)row * ldc + col;
-                *cp = mode == GEMM_ADD ? *cp + acc[t][i] : acc[t][i];
+                    for (int r = 0; r < 4; ++r) acc[i][t][r] += sc * tmp[i][t][r];
             }
         }
+        if (more) {
+            store_a(buf ^ 1);
+#pragma unroll
+            for (int i = 0; i < NBW; ++i) {
+#pragma unroll
+                for (int j = 0; j < WV; ++j) wcur[i][j] = wnext[i][j];
+                scur[i] = snext[i];
+            }
+        }
+        __syncthreads();
     }
+
+    // ---- epilogue
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+        const int col = (nb0 + i) * 16 + (lane & 15);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + t * 16 + (lane >> 4) * 4 + r;
+                if (row >= M) continue;
+                if (S == 1) {
+                    float* cp = C + (size_t)row * ldc + col;
+                    *cp = mode == GEMM_ADD ? *cp + acc[i][t][r] : acc[i][t][r];
+                } else {
+                    P[((size_t)s * M + row) * N + col] = acc[i][t][r];
+                }
+            }
+    }
+}
+
+// C[m][n] (+)= sum_s P[s][m][n]
+__global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__ P, float* __restrict__ C, int M, int N,
+                                                       int ldc, int S, int mode)
+{
+    size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+    size_t MN = (size_t)M * N;
+    if (idx >= MN) return;
+    float v = 0.f;
+    for (int s = 0; s < S; ++s) v += P[(size_t)s * MN + idx];
+    int row = (int)(idx / N), col = (int)(idx % N);
+    float* cp = C + (size_t)row * ldc + col;
+    *cp = mode == GEMM_ADD ? *cp + v : v;
 }
 
 // ------------------------------------------------------------------ int4 x fp32 VALU
@@ -245,11 +287,58 @@ __global__ void __launch_bounds__(256) k_gemm_q4_f32(const float* __restrict__ A
 
 }  // namespace
 
-void launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N, int K, int ldc, gemm_mode mode,
-                      hipStream_t s)
+void gemm_plan(int M, int N, int K, int* nbw, int* S)
 {
-    dim3 grid(N / BN, (M + BM - 1) / BM);
-    k_gemm_bf16<<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, mode);
+    *nbw = (N % 128 == 0) ? 2 : 1;
+    int tiles = N / (64 * *nbw);
+    int msup = (M + SM - 1) / SM;
+    int G = K / SK;
+    int s = 1;
+    while (tiles * s * msup < 512 && G % (2 * s) == 0 && G / (2 * s) >= 2 && 2 * s <= 8) s *= 2;
+    *S = s;
+}
+
+size_t gemm_part_floats(int M, int N, int K)
+{
+    int nbw, S;
+    gemm_plan(M, N, K, &nbw, &S);
+    return S > 1 ? (size_t)S * M * N : 0;
+}
+
+template <int WF, int NBW>
+static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C,
+                      float* P, int M, int N, int K, int ldc, int mode, int S, int msup, int total)
+{
+    switch (MT) {
+        case 1: k_gemm_stream<WF, NBW, 1><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 2: k_gemm_stream<WF, NBW, 2><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 3: k_gemm_stream<WF, NBW, 3><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        default: k_gemm_stream<WF, NBW, 4><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
+    }
+}
+
+void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
+                        size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s)
+{
+    int nbw, S;
+    gemm_plan(M, N, K, &nbw, &S);
+    if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
+    int msup = (M + SM - 1) / SM;
+    int MT = msup > 1 ? 4 : (M + 15) / 16;
+    int tiles = N / (64 * nbw);
+    int total = tiles * S * msup;
+    dim3 grid((total + 7) / 8 * 8);
+    if (wf == 0) {
+        if (nbw == 2) stream_mt<0, 2>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
+        else stream_mt<0, 1>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
+    } else {
+        if (nbw == 2) stream_mt<1, 2>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
+        else stream_mt<1, 1>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
+    }
+    if (S > 1) {
+        size_t MN = (size_t)M * N;
+        k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
+    }
 }
 
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, gemm_mode mode,
@@ -257,13 +346,6 @@ void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int
 {
     dim3 grid(N / FT, (M + FT - 1) / FT);
     k_gemm_f32<<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, mode);
-}
-
-void launch_gemm_q4_f16(const _Float16* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M, int N, int K,
-                        int ldc, gemm_mode mode, hipStream_t s)
-{
-    dim3 grid(N / 16, (M + 63) / 64);
-    k_gemm_q4_f16<<<grid, 64, 0, s>>>(A, Wq, Sc, C, M, N, K, ldc, mode);
 }
 
 void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M, int N, int K,

@@ -226,15 +226,220 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
     }
 }
 
+// MFMA attention for a bf16 cache.  Work-group (b, kv head, chunk of MCH
+// positions, query-row slice z); each wave takes a quarter of the chunk in
+// blocks of 32 positions.  Per block:
+//   S^T = K Q^T with v_mfma_f32_16x16x32_bf16: K rows straight from global
+//   memory (lane l: position l%16 of a 16-row tile, dims 8*(4ks + l/16)+0..7),
+//   Q^T pre-scaled by log2(e)/sqrt(d).  Lane l then holds the scores of query
+//   row l%16 at positions 4*(l/16) + r and 16 + 4*(l/16) + r (r = 0..3), which
+//   is exactly the B operand layout of the next product, so P never leaves
+//   registers.
+//   O^T += V^T P^T: V is staged row-major in a wave-private LDS tile (row
+//   stride d + 8, bank-conflict free for the gather) and read transposed.
+// The online softmax runs per query row in base 2; the four waves are merged
+// through LDS and the chunk result (m in natural-log units, l, o[d]) goes to
+// the same partial buffer k_attn_combine reads.
+constexpr int MCH = 512;
+
+template <int D, int MQ>
+__global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
+                                                   const uint16_t* vc, int layer, float* part, int max_chunks)
+{
+    constexpr int KS = D / 32;      // k-steps over the head dim
+    constexpr int NBD = D / 16;     // 16-wide blocks of the head dim
+    constexpr int LDV = D + 8;      // LDS row stride (elements)
+    constexpr int CPP = D / 8;      // 16-byte pieces per cached position
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[4][32 * LDV];
+    __shared__ float s_ml[4][2][16];
+
+    const int b = blockIdx.x / n_kv, kvh = blockIdx.x - b * n_kv;
+    const int c = blockIdx.y, z = blockIdx.z;
+    const int slot = r.slots[b];
+    if (slot < 0 || slot >= r.max_slots) return;   // flagged by k_rope_kv
+    const int basepos = r.kv_len[slot] + r.off;
+    int ctx = basepos + r.n;
+    if (ctx > r.max_ctx) ctx = r.max_ctx;
+    const int p0 = c * MCH;
+    if (p0 >= ctx) return;
+    const int p1 = min(p0 + MCH, ctx);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int cq = lane >> 4, lr = lane & 15;
+    const int G = n_q / n_kv, QR = G * r.n;
+    const int qbase = z * 16 * MQ;
+
+    // Q^T fragments (B operand of S^T = K Q^T)
+    const float qscale = 1.4426950408889634f * rsqrtf((float)D);
+    bf16x8 qf[MQ][KS];
+    int lim[MQ];
+#pragma unroll
+    for (int mt = 0; mt < MQ; ++mt) {
+        const int qrow = qbase + 16 * mt + lr;
+        const bool live = qrow < QR;
+        const int g = live ? qrow / r.n : 0, i = live ? qrow - g * r.n : 0;
+        lim[mt] = live ? basepos + i : -1;
+        const float* qp = q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            uint16_t h[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = live ? f32_to_bf16(qp[8 * (4 * ks + cq) + e] * qscale) : 0;
+            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
+                                                             h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16)});
+        }
+    }
+
+    const size_t cbase = ((((size_t)layer * r.max_slots + slot) * n_kv + kvh) * (size_t)r.max_ctx) * D;
+    const uint16_t* K = kc + cbase;
+    const uint16_t* V = vc + cbase;
+    uint16_t* vs = Vs[w];
+
+    float m[MQ], lsum[MQ];
+    floatx4 o[MQ][NBD];
+#pragma unroll
+    for (int mt = 0; mt < MQ; ++mt) {
+        m[mt] = -INFINITY;
+        lsum[mt] = 0.f;
+#pragma unroll
+        for (int nb = 0; nb < NBD; ++nb) o[mt][nb] = (floatx4){0.f, 0.f, 0.f, 0.f};
+    }
+
+    const int wq0 = p0 + w * (MCH / 4), wq1 = min(p0 + (w + 1) * (MCH / 4), p1);
+    for (int blk = wq0; blk < wq1; blk += 32) {
+        // V block -> wave-private LDS tile (row-major, padded)
+#pragma unroll
+        for (int t = 0; t < CPP / 2; ++t) {
+            const int piece = t * 64 + lane;
+            const int pos = piece / CPP, ch = piece - pos * CPP;
+            u32x4 val = (blk + pos < wq1) ? *(const u32x4*)(V + (size_t)(blk + pos) * D + ch * 8) : (u32x4){0u, 0u, 0u, 0u};
+            *(u32x4*)(vs + pos * LDV + ch * 8) = val;
+        }
+        // K fragments for the two 16-position tiles
+        u32x4 kf[2][KS];
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt) {
+            const int pos = blk + 16 * pt + lr;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                kf[pt][ks] = pos < wq1 ? *(const u32x4*)(K + (size_t)pos * D + 8 * (4 * ks + cq)) : (u32x4){0u, 0u, 0u, 0u};
+        }
+        bf16x8 pf[MQ];
+#pragma unroll
+        for (int mt = 0; mt < MQ; ++mt) {
+            floatx4 st[2];
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt) {
+                st[pt] = (floatx4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    st[pt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[pt][ks]), qf[mt][ks],
+                                                                     st[pt], 0, 0, 0);
+            }
+            float bm = -INFINITY;
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int pos = blk + 16 * pt + 4 * cq + i;
+                    float sv = st[pt][i];
+                    if (pos >= wq1 || pos > lim[mt]) sv = -INFINITY;
+                    st[pt][i] = sv;
+                    bm = fmaxf(bm, sv);
+                }
+            bm = fmaxf(bm, __shfl_xor(bm, 16, WAVE));
+            bm = fmaxf(bm, __shfl_xor(bm, 32, WAVE));
+            const float mn = fmaxf(m[mt], bm);
+            const float corr = m[mt] == -INFINITY ? 0.f : exp2f(m[mt] - mn);
+            m[mt] = mn;
+            lsum[mt] *= corr;
+#pragma unroll
+            for (int nb = 0; nb < NBD; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[mt][nb][i] *= corr;
+            uint16_t ph[8];
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float x = st[pt][i];
+                    const float pv = x == -INFINITY ? 0.f : exp2f(x - mn);
+                    lsum[mt] += pv;
+                    ph[pt * 4 + i] = f32_to_bf16(pv);
+                }
+            pf[mt] = __builtin_bit_cast(bf16x8, (u32x4){ph[0] | ((uint32_t)ph[1] << 16), ph[2] | ((uint32_t)ph[3] << 16),
+                                                        ph[4] | ((uint32_t)ph[5] << 16), ph[6] | ((uint32_t)ph[7] << 16)});
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // O^T += V^T P^T
+#pragma unroll
+        for (int nb = 0; nb < NBD; ++nb) {
+            uint16_t vh[8];
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) vh[pt * 4 + i] = vs[(16 * pt + 4 * cq + i) * LDV + 16 * nb + lr];
+            const bf16x8 vt = __builtin_bit_cast(bf16x8, (u32x4){vh[0] | ((uint32_t)vh[1] << 16), vh[2] | ((uint32_t)vh[3] << 16),
+                                                                 vh[4] | ((uint32_t)vh[5] << 16), vh[6] | ((uint32_t)vh[7] << 16)});
+#pragma unroll
+            for (int mt = 0; mt < MQ; ++mt) o[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pf[mt], o[mt][nb], 0, 0, 0);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+#pragma unroll
+    for (int mt = 0; mt < MQ; ++mt) {
+        lsum[mt] += __shfl_xor(lsum[mt], 16, WAVE);
+        lsum[mt] += __shfl_xor(lsum[mt], 32, WAVE);
+    }
+
+    // merge the four waves, 16 query rows at a time, through the (now free) V tiles
+    float* so = (float*)&Vs[0][0];   // [4 waves][16 rows][D]
+    const float LN2 = 0.6931471805599453f;
+    for (int mt = 0; mt < MQ; ++mt) {
+        __syncthreads();
+        if (cq == 0) { s_ml[w][0][lr] = m[mt]; s_ml[w][1][lr] = lsum[mt]; }
+#pragma unroll
+        for (int nb = 0; nb < NBD; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) so[(w * 16 + lr) * D + 16 * nb + 4 * cq + i] = o[mt][nb][i];
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < 16 * D; idx += 256) {
+            const int qr = idx / D, d = idx - qr * D;
+            const int qrow = qbase + 16 * mt + qr;
+            if (qrow >= QR) continue;
+            float mm = -INFINITY;
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww) mm = fmaxf(mm, s_ml[ww][0][qr]);
+            float ls = 0.f, os = 0.f;
+            if (mm > -INFINITY) {
+#pragma unroll
+                for (int ww = 0; ww < 4; ++ww) {
+                    const float mw = s_ml[ww][0][qr];
+                    const float f = mw > -INFINITY ? exp2f(mw - mm) : 0.f;
+                    ls += s_ml[ww][1][qr] * f;
+                    os += so[(ww * 16 + qr) * D + d] * f;
+                }
+            }
+            const int g = qrow / r.n, i = qrow - g * r.n;
+            float* pp = part + (((size_t)(b * r.n + i) * n_q + kvh * G + g) * max_chunks + c) * (D + 2);
+            if (d == 0) { pp[0] = mm * LN2; pp[1] = ls; }
+            pp[2 + d] = os;
+        }
+    }
+}
+
 template <typename O>
-__global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int max_chunks, void* out)
+__global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int max_chunks, int chunk, void* out)
 {
     int row = blockIdx.x / n_q, hq = blockIdx.x - row * n_q;
     int b = row / r.n;
     int slot = r.slots[b];
     int ctx = 0;
     if (slot >= 0 && slot < r.max_slots) ctx = min(r.kv_len[slot] + r.off + r.n, r.max_ctx);
-    int nch = (ctx + ATT_CH - 1) / ATT_CH;
+    int nch = (ctx + chunk - 1) / chunk;
     if (nch > max_chunks) nch = max_chunks;
     const float* pp = part + ((size_t)row * n_q + hq) * max_chunks * (D + 2);
     for (int k = threadIdx.x; k < D; k += blockDim.x) {
@@ -331,7 +536,7 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float2* rope, int n
                                               (uint16_t*)c.v, layer, q_out);
 }
 
-int attention_chunk() { return ATT_CH; }
+int attention_chunk() { return ATT_CH < MCH ? ATT_CH : MCH; }
 
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
 {
@@ -342,12 +547,32 @@ template <typename T, int D>
 static void attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
                    int max_chunks, void* out, act_t out_t, hipStream_t s)
 {
-    dim3 grid(r.B * c.n_kv, max_chunks);
-    k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
+    int chunk = ATT_CH;
+    if constexpr (sizeof(T) == 2) {
+        // bf16 cache: MFMA kernel, chunks of MCH positions (max_chunks counts ATT_CH chunks, ATT_CH <= MCH)
+        const int QR = (n_q / c.n_kv) * r.n;
+        const int MQ = QR > 48 ? 4 : (QR + 15) / 16;
+        const int zs = (QR + 16 * MQ - 1) / (16 * MQ);
+        const int mch = (max_chunks * ATT_CH + MCH - 1) / MCH;
+        dim3 grid(r.B * c.n_kv, mch, zs);
+        const uint16_t* kc = (const uint16_t*)c.k;
+        const uint16_t* vc = (const uint16_t*)c.v;
+        switch (MQ) {
+            case 1: k_attn_mfma<D, 1><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
+            case 2: k_attn_mfma<D, 2><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
+            case 3: k_attn_mfma<D, 3><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
+            default: k_attn_mfma<D, 4><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
+        }
+        max_chunks = mch;
+        chunk = MCH;
+    } else {
+        dim3 grid(r.B * c.n_kv, max_chunks);
+        k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
+    }
     int R = r.B * r.n;
-    if (out_t == ACT_F32) k_attn_combine<float><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
-    else if (out_t == ACT_BF16) k_attn_combine<uint16_t><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
-    else k_attn_combine<_Float16><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, out);
+    if (out_t == ACT_F32) k_attn_combine<float><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
+    else if (out_t == ACT_BF16) k_attn_combine<uint16_t><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
+    else k_attn_combine<_Float16><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
 }
 
 void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,

@@ -28,8 +28,12 @@ API_SYMBOLS = (
     "sd_bind_kv", "sd_drafter_bytes", "sd_refresh_drafter", "sd_prefill", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
-    "sd_alpha_from_tau",
+    "sd_alpha_from_tau", "sd_timing", "sd_timing_read",
 )
+
+# kernel classes of sd_timing_read
+T_ATTN, T_Q4, T_PROJ, T_LMHEAD, T_SAMPLE, T_ACCEPT, T_MISC = range(7)
+T_NAMES = ("attention", "int4_proj", "bf16_proj", "lm_head", "sampler", "accept", "misc")
 
 
 class SDError(RuntimeError):
@@ -89,6 +93,8 @@ def lib():
             "sd_ar_step": (_i32, [_P, _i32, _P, _P, _f, Rng, _P, _P, _P]),
             "sd_sync": (_i32, [_P, _P]),
             "sd_set_debug": (_i32, [_P, _i32]),
+            "sd_timing": (_i32, [_P, _i32]),
+            "sd_timing_read": (_i32, [_P, _i32, _P, _P]),
             "sd_cost_init": (_i32, [_P, _d, _d, _d, _P]),
             "sd_cost_times": (_i32, [_P, _d, _d, _i32, _P, _P, _P]),
             "sd_toggle": (_i32, [_P, _i32, _d, _d, _i32, _d, _P]),
@@ -271,6 +277,14 @@ class Engine:
 
     def sync(self):
         _check(lib().sd_sync(self.h, _stream()))
+
+    def timing(self, on: bool):
+        _check(lib().sd_timing(self.h, 1 if on else 0))
+
+    def timing_read(self, cls: int):
+        ms, n = C.c_double(), C.c_int32()
+        _check(lib().sd_timing_read(self.h, cls, C.byref(ms), C.byref(n)))
+        return ms.value, n.value
 
 
 class SDBuffers:

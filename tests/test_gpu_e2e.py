@@ -133,7 +133,7 @@ SMALL_GQA = dict(name="small-gqa-bf16", n_layers=2, hidden=512, n_q=4, n_kv=2, h
                  vocab=2048, dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
 
 
-@pytest.mark.parametrize("ctx_fill", [0, 300], ids=["prefill", "random-context"])
+@pytest.mark.parametrize("ctx_fill", [0, 300, 1100], ids=["prefill", "random-context", "long-context"])
 def test_small_bf16_sd_matches_oracle(ctx_fill):
     cfg = SMALL_GQA
     say("small bf16 SD", ctx_fill)
@@ -145,4 +145,38 @@ def test_small_bf16_sd_matches_oracle(ctx_fill):
     say("stats", st)
     assert st["ok"] >= 3 * B
     assert st["exempt"] <= 2
+    eng.close()
+
+
+def test_small_bf16_long_prefill_then_ar():
+    """One sequence prefilled in chunks of 40 tokens (80 query rows per
+    attention work-group slice set), then AR steps: logits, tokens and cache
+    against the oracle."""
+    cfg = SMALL_GQA
+    say("small bf16 long prefill + AR")
+    P, T, seed, step = 97, 1.0, 8, 2
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(1, P, cfg["vocab"], seed)
+    eng, k, v, kv_len = make_engine(cfg, [w.cuda() for w in W], 8, 160, 4)
+    target, _ = oracle_models(cfg, host_bits(W))
+    okv = oracle.KV(cfg, 160)
+    slot = 5
+    eng.prefill(i32([slot]), prompt[:, :P - 1].cuda())
+    oracle.forward_seq(target, okv, prompt[0, :P - 1].numpy(), 0, want_logits=False)
+    eng.sync()
+    kd = k[:, slot, :, : P - 1].float().cpu().numpy()
+    vd = v[:, slot, :, : P - 1].float().cpu().numpy()
+    assert np.abs(kd - okv.k[:, :, : P - 1]).max() <= 2e-2 * np.abs(okv.k[:, :, : P - 1]).max()
+    assert np.abs(vd - okv.v[:, :, : P - 1]).max() <= 2e-2 * np.abs(okv.v[:, :, : P - 1]).max()
+    last = int(prompt[0, P - 1])
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pl = torch.zeros((1, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    for t in range(6):
+        eng.ar_step(i32([slot]), i32([last]), T, seed, step, out, pl)
+        eng.sync()
+        x, p, gap = oracle.ar_step_seq(target, okv, P - 1 + t, last, T, seed, step, slot)
+        status = compare_ar(x, gap, p, int(out.cpu()[0]), pl.cpu().numpy()[0], 2e-2, T)
+        if status == "exempt":
+            break
+        last = x
     eng.close()
