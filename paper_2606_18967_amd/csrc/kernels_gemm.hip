@@ -108,6 +108,9 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
                                                      float* __restrict__ P, int M, int N, int K, int ldc, int mode,
                                                      int S, int msup, int total)
 {
+    // weights are prefetched RD - 1 chunks ahead through a ring of register sets
+    constexpr int RD = WF == 0 ? 4 : 3;
+    constexpr int WV = WF == 0 ? 1 : 4;                     // 16-byte vectors per lane per block per chunk
     __shared__ __attribute__((aligned(16))) uint16_t As[2][SM * ALD];
     const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
@@ -120,41 +123,38 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     const int nb0 = (tile * 4 + wv) * NBW;
     const int rows = min(M - m0, MT * 16);                  // rows staged (others stay zero)
 
-    // ---- loaders
     u32x4 a_reg[4];
     auto load_a = [&](int g) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            int pidx = tid + t * 256;
-            int row = pidx >> 4, col = (pidx & 15) * 8;
-            a_reg[t] = (row < rows) ? *(const u32x4*)(A + (size_t)(m0 + row) * K + (size_t)g * SK + col)
-                                    : (u32x4){0u, 0u, 0u, 0u};
+            const int pidx = tid + t * 256;
+            const int row = pidx >> 4, col = (pidx & 15) * 8;
+            a_reg[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)g * SK + col);
         }
     };
     auto store_a = [&](int buf) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            int pidx = tid + t * 256;
-            int row = pidx >> 4, col = (pidx & 15) * 8;
-            if (row < MT * 16) *(u32x4*)(&As[buf][row * ALD + col]) = a_reg[t];
+            const int pidx = tid + t * 256;
+            const int row = pidx >> 4, col = (pidx & 15) * 8;
+            if (row < MT * 16) *(u32x4*)(&As[buf][row * ALD + col]) = row < rows ? a_reg[t] : (u32x4){0u, 0u, 0u, 0u};
         }
     };
-    constexpr int WV = WF == 0 ? 1 : 4;                     // 16-byte vectors per lane per block per chunk
-    u32x4 wcur[NBW][WV], wnext[NBW][WV];
-    uint16_t scur[NBW], snext[NBW];
-    auto load_w = [&](int g, u32x4 (&wr)[NBW][WV], uint16_t (&sr)[NBW]) {
+    u32x4 wr[RD][NBW][WV];
+    uint16_t sr[RD][NBW];
+    auto load_w = [&](int g, u32x4 (&wq)[NBW][WV], uint16_t (&sq)[NBW]) {
 #pragma unroll
         for (int i = 0; i < NBW; ++i) {
-            int nb = nb0 + i;
+            const int nb = nb0 + i;
             if constexpr (WF == 0) {
-                wr[i][0] = ((const u32x4*)Wt)[((size_t)nb * G + g) * 64 + lane];
-                sr[i] = Sc[((size_t)nb * G + g) * 16 + (lane & 15)];
+                wq[i][0] = ((const u32x4*)Wt)[((size_t)nb * G + g) * 64 + lane];
+                sq[i] = Sc[((size_t)nb * G + g) * 16 + (lane & 15)];
             } else {
                 const uint16_t* wp = (const uint16_t*)Wt + (size_t)(nb * 16 + (lane & 15)) * K + (size_t)g * SK +
                                      32 * (lane >> 4);
 #pragma unroll
-                for (int j = 0; j < WV; ++j) wr[i][j] = *(const u32x4*)(wp + 8 * j);
-                sr[i] = 0;
+                for (int j = 0; j < WV; ++j) wq[i][j] = *(const u32x4*)(wp + 8 * j);
+                sq[i] = 0;
             }
         }
     };
@@ -165,34 +165,26 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
 #pragma unroll
         for (int t = 0; t < MT; ++t) acc[i][t] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
-    load_w(g0, wcur, scur);
-    load_a(g0);
-    store_a(0);
-    __syncthreads();
-
-    for (int g = g0; g < g1; ++g) {
-        const int buf = (g - g0) & 1;
-        const bool more = g + 1 < g1;
-        if (more) { load_w(g + 1, wnext, snext); load_a(g + 1); }
+    auto compute = [&](int buf, const u32x4 (&wq)[NBW][WV], const uint16_t (&sq)[NBW]) {
         floatx4 tmp[NBW][MT];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int acol = WF == 0 ? 32 * j + 8 * (lane >> 4) : 32 * (lane >> 4) + 8 * j;
-            uint16_t* ab = &As[buf][(lane & 15) * ALD + acol];
+            const uint16_t* ab = &As[buf][(lane & 15) * ALD + acol];
             u32x4 af[MT];
 #pragma unroll
             for (int t = 0; t < MT; ++t) af[t] = *(const u32x4*)(ab + t * 16 * ALD);
 #pragma unroll
             for (int i = 0; i < NBW; ++i) {
                 if constexpr (WF == 0) {
-                    half8 bq = dequant8(wcur[i][0][j]);
+                    const half8 bq = dequant8(wq[i][0][j]);
 #pragma unroll
                     for (int t = 0; t < MT; ++t)
                         tmp[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                             __builtin_bit_cast(half8, af[t]), bq, j == 0 ? (floatx4){0.f, 0.f, 0.f, 0.f} : tmp[i][t],
                             0, 0, 0);
                 } else {
-                    bf16x8 bb = __builtin_bit_cast(bf16x8, wcur[i][j]);
+                    const bf16x8 bb = __builtin_bit_cast(bf16x8, wq[i][j]);
 #pragma unroll
                     for (int t = 0; t < MT; ++t)
                         acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[t]), bb,
@@ -203,23 +195,39 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
         if constexpr (WF == 0) {
 #pragma unroll
             for (int i = 0; i < NBW; ++i) {
-                float sc = f16_bits_to_f32(scur[i]);
+                const float sc = f16_bits_to_f32(sq[i]);
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) acc[i][t][r] += sc * tmp[i][t][r];
             }
         }
-        if (more) {
-            store_a(buf ^ 1);
+    };
+
+    // prologue: A of chunk g0 into LDS, weights of the first RD - 1 chunks in flight
+    load_a(g0);
 #pragma unroll
-            for (int i = 0; i < NBW; ++i) {
+    for (int u = 0; u < RD - 1; ++u)
+        if (g0 + u < g1) load_w(g0 + u, wr[u], sr[u]);
+    store_a(0);
+    __syncthreads();
+
+    // chunk c uses ring slot (c - g0) % RD; at chunk c the A tile of c + 1 and
+    // the weights of c + RD - 1 are requested (A first, so waiting for it
+    // leaves the newer weight loads in flight)
+    for (int gb = g0; gb < g1; gb += RD) {
 #pragma unroll
-                for (int j = 0; j < WV; ++j) wcur[i][j] = wnext[i][j];
-                scur[i] = snext[i];
+        for (int u = 0; u < RD; ++u) {
+            const int c = gb + u;
+            if (c < g1) {
+                const int buf = (c - g0) & 1;
+                if (c + 1 < g1) load_a(c + 1);
+                if (c + RD - 1 < g1) load_w(c + RD - 1, wr[(u + RD - 1) % RD], sr[(u + RD - 1) % RD]);
+                compute(buf, wr[u], sr[u]);
+                if (c + 1 < g1) store_a(buf ^ 1);
+                __syncthreads();
             }
         }
-        __syncthreads();
     }
 
     // ---- epilogue
@@ -240,6 +248,121 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
                 }
             }
     }
+}
+
+// ------------------------------------------------------------------ tiled bf16 MFMA GEMM (M > 64)
+// C[M][N] = A[M][K] W^T with both operands staged through LDS.  Block tile
+// (32*MTW) x 128, four waves in a 2 x 2 grid, each wave (16*MTW) x 64 =
+// MTW x 4 MFMA tiles of v_mfma_f32_16x16x32_bf16.  K advances in stages of 64
+// with double-buffered LDS and the global loads of stage k + 2 in flight while
+// stage k is multiplied.  LDS rows are padded to 72 elements (bank-conflict
+// free 16-byte fragment reads).  Split-K partials as in k_gemm_stream.
+constexpr int TBK = 64, TLD = TBK + 8, TBN = 128;
+
+template <int MTW>
+__global__ void __launch_bounds__(256) k_gemm_tiled(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+                                                    float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
+                                                    int ldc, int mode, int S, int mtiles, int total)
+{
+    constexpr int BM = 32 * MTW;
+    constexpr int AP = MTW;      // 16-byte A pieces per thread per stage (BM*8/256)
+    constexpr int WP = 4;        // 16-byte W pieces per thread per stage (128*8/256)
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * TLD];
+    __shared__ __attribute__((aligned(16))) uint16_t Ws[2][TBN * TLD];
+    const int per_xcd = gridDim.x >> 3;
+    const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (w >= total) return;
+    const int mt = w % mtiles, rest = w / mtiles;
+    const int s = rest % S, nt = rest / S;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1;
+    const int m0 = mt * BM, n0 = nt * TBN;
+    const int KS = K / TBK, Ks = KS / S, k0 = s * Ks, k1 = k0 + Ks;
+    const int rows = min(M - m0, BM);
+
+    u32x4 ra[2][AP], rw[2][WP];
+    auto load = [&](int kb, u32x4 (&a)[AP], u32x4 (&b)[WP]) {
+#pragma unroll
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            a[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)kb * TBK + col);
+        }
+#pragma unroll
+        for (int t = 0; t < WP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            b[t] = *(const u32x4*)(W + (size_t)(n0 + row) * K + (size_t)kb * TBK + col);
+        }
+    };
+    auto store = [&](int buf, const u32x4 (&a)[AP], const u32x4 (&b)[WP]) {
+#pragma unroll
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            *(u32x4*)(&As[buf][row * TLD + col]) = row < rows ? a[t] : (u32x4){0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int t = 0; t < WP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            *(u32x4*)(&Ws[buf][row * TLD + col]) = b[t];
+        }
+    };
+
+    floatx4 acc[MTW][4];
+#pragma unroll
+    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = (floatx4){0.f, 0.f, 0.f, 0.f};
+
+    load(k0, ra[0], rw[0]);
+    if (k0 + 1 < k1) load(k0 + 1, ra[1], rw[1]);
+    store(0, ra[0], rw[0]);
+    __syncthreads();
+    for (int kb = k0; kb < k1; kb += 2) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int k = kb + u;
+            if (k < k1) {
+                const int buf = (k - k0) & 1;
+                if (k + 2 < k1) load(k + 2, ra[u], rw[u]);      // slot u is free: stage k is in LDS
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int kk = ks * 32 + (lane >> 4) * 8;
+                    u32x4 af[MTW], bw[4];
+#pragma unroll
+                    for (int i = 0; i < MTW; ++i)
+                        af[i] = *(const u32x4*)(&As[buf][(wm * 16 * MTW + 16 * i + (lane & 15)) * TLD + kk]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        bw[j] = *(const u32x4*)(&Ws[buf][(wn * 64 + 16 * j + (lane & 15)) * TLD + kk]);
+#pragma unroll
+                    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[i]),
+                                                                               __builtin_bit_cast(bf16x8, bw[j]),
+                                                                               acc[i][j], 0, 0, 0);
+                }
+                if (k + 1 < k1) store(buf ^ 1, ra[u ^ 1], rw[u ^ 1]);
+                __syncthreads();
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = n0 + wn * 64 + 16 * j + (lane & 15);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + wm * 16 * MTW + 16 * i + (lane >> 4) * 4 + r;
+                if (row >= M) continue;
+                if (S == 1) {
+                    float* cp = C + (size_t)row * ldc + col;
+                    *cp = mode == GEMM_ADD ? *cp + acc[i][j][r] : acc[i][j][r];
+                } else {
+                    P[((size_t)s * M + row) * N + col] = acc[i][j][r];
+                }
+            }
+        }
 }
 
 // C[m][n] (+)= sum_s P[s][m][n]
@@ -287,6 +410,15 @@ __global__ void __launch_bounds__(256) k_gemm_q4_f32(const float* __restrict__ A
 
 }  // namespace
 
+// Split-K is used until the launch has GEMM_SPLIT_TARGET work-groups, with at
+// most GEMM_MAX_SPLIT splits and at least two chunks per split.
+#ifndef GEMM_SPLIT_TARGET
+#define GEMM_SPLIT_TARGET 256
+#endif
+#ifndef GEMM_MAX_SPLIT
+#define GEMM_MAX_SPLIT 8
+#endif
+
 void gemm_plan(int M, int N, int K, int* nbw, int* S)
 {
     *nbw = (N % 128 == 0) ? 2 : 1;
@@ -294,7 +426,28 @@ void gemm_plan(int M, int N, int K, int* nbw, int* S)
     int msup = (M + SM - 1) / SM;
     int G = K / SK;
     int s = 1;
-    while (tiles * s * msup < 512 && G % (2 * s) == 0 && G / (2 * s) >= 2 && 2 * s <= 8) s *= 2;
+    while (tiles * s * msup < GEMM_SPLIT_TARGET && G % (2 * s) == 0 && G / (2 * s) >= 2 && 2 * s <= GEMM_MAX_SPLIT)
+        s *= 2;
+    *S = s;
+}
+
+// bf16 GEMMs with more than 64 rows use the tiled kernel (N % 128 == 0).
+static bool use_tiled(int wf, int M, int N, int K) { return wf == 1 && M > 64 && N % TBN == 0 && K % TBK == 0; }
+
+static int tiled_mtw(int M)
+{
+    (void)M;
+    return 4;   // 128-row tiles: two work-groups per CU (the 160-row variant fits one)
+}
+
+static void tiled_plan(int M, int N, int K, int* mtw, int* S)
+{
+    *mtw = tiled_mtw(M);
+    int mtiles = (M + 32 * *mtw - 1) / (32 * *mtw);
+    int tiles = N / TBN * mtiles;
+    int KS = K / TBK;
+    int s = 1;
+    while (tiles * s < GEMM_SPLIT_TARGET && KS % (2 * s) == 0 && KS / (2 * s) >= 4 && 2 * s <= GEMM_MAX_SPLIT) s *= 2;
     *S = s;
 }
 
@@ -302,6 +455,11 @@ size_t gemm_part_floats(int M, int N, int K)
 {
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
+    if (use_tiled(1, M, N, K)) {
+        int mtw, St;
+        tiled_plan(M, N, K, &mtw, &St);
+        S = St > S ? St : S;
+    }
     return S > 1 ? (size_t)S * M * N : 0;
 }
 
@@ -320,6 +478,21 @@ static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const
 void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
                         size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s)
 {
+    if (use_tiled(wf, M, N, K)) {
+        int mtw, S;
+        tiled_plan(M, N, K, &mtw, &S);
+        if (S > 1 && (size_t)S * M * N > part_cap) S = 1;
+        int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
+        int total = N / TBN * mtiles * S;
+        dim3 grid((total + 7) / 8 * 8);
+        const uint16_t* W = (const uint16_t*)Wt;
+        k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
+        if (S > 1) {
+            size_t MN = (size_t)M * N;
+            k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
+        }
+        return;
+    }
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
     if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split

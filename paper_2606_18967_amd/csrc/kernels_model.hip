@@ -240,7 +240,10 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 // The online softmax runs per query row in base 2; the four waves are merged
 // through LDS and the chunk result (m in natural-log units, l, o[d]) goes to
 // the same partial buffer k_attn_combine reads.
-constexpr int MCH = 512;
+#ifndef ATT_MFMA_CHUNK
+#define ATT_MFMA_CHUNK 1024
+#endif
+constexpr int MCH = ATT_MFMA_CHUNK;   // positions per work-group
 
 template <int D, int MQ>
 __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
@@ -268,7 +271,7 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
     const int G = n_q / n_kv, QR = G * r.n;
     const int qbase = z * 16 * MQ;
 
-    // Q^T fragments (B operand of S^T = K Q^T)
+    // Q^T fragments (B operand of S^T = K Q^T); rows past QR read row 0 and are zeroed
     const float qscale = 1.4426950408889634f * rsqrtf((float)D);
     bf16x8 qf[MQ][KS];
     int lim[MQ];
@@ -276,16 +279,22 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
     for (int mt = 0; mt < MQ; ++mt) {
         const int qrow = qbase + 16 * mt + lr;
         const bool live = qrow < QR;
-        const int g = live ? qrow / r.n : 0, i = live ? qrow - g * r.n : 0;
+        const int qr = live ? qrow : 0;
+        const int g = qr / r.n, i = qr - g * r.n;
         lim[mt] = live ? basepos + i : -1;
-        const float* qp = q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D;
+        const float sc = live ? qscale : 0.f;
+        const float4* qp = (const float4*)(q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D);
+        float4 qv[KS][2];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            uint16_t h[8];
+            qv[ks][0] = qp[2 * (4 * ks + cq)];
+            qv[ks][1] = qp[2 * (4 * ks + cq) + 1];
+        }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) h[e] = live ? f32_to_bf16(qp[8 * (4 * ks + cq) + e] * qscale) : 0;
-            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
-                                                             h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16)});
+        for (int ks = 0; ks < KS; ++ks) {
+            const float4 a = qv[ks][0], c2 = qv[ks][1];
+            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){pack_bf16x2(a.x * sc, a.y * sc), pack_bf16x2(a.z * sc, a.w * sc),
+                                                            pack_bf16x2(c2.x * sc, c2.y * sc), pack_bf16x2(c2.z * sc, c2.w * sc)});
         }
     }
 
@@ -306,22 +315,27 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
 
     const int wq0 = p0 + w * (MCH / 4), wq1 = min(p0 + (w + 1) * (MCH / 4), p1);
     for (int blk = wq0; blk < wq1; blk += 32) {
-        // V block -> wave-private LDS tile (row-major, padded)
+        // K fragments for the two 16-position tiles, then the V block; positions
+        // past the wave's range read its last position and are zeroed
+        u32x4 kf[2][KS];
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt) {
+            const int pos = min(blk + 16 * pt + lr, wq1 - 1);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kf[pt][ks] = *(const u32x4*)(K + (size_t)pos * D + 8 * (4 * ks + cq));
+        }
+        u32x4 vv[CPP / 2];
 #pragma unroll
         for (int t = 0; t < CPP / 2; ++t) {
             const int piece = t * 64 + lane;
             const int pos = piece / CPP, ch = piece - pos * CPP;
-            u32x4 val = (blk + pos < wq1) ? *(const u32x4*)(V + (size_t)(blk + pos) * D + ch * 8) : (u32x4){0u, 0u, 0u, 0u};
-            *(u32x4*)(vs + pos * LDV + ch * 8) = val;
+            vv[t] = *(const u32x4*)(V + (size_t)min(blk + pos, wq1 - 1) * D + ch * 8);
         }
-        // K fragments for the two 16-position tiles
-        u32x4 kf[2][KS];
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt) {
-            const int pos = blk + 16 * pt + lr;
+            const bool ok = blk + 16 * pt + lr < wq1;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                kf[pt][ks] = pos < wq1 ? *(const u32x4*)(K + (size_t)pos * D + 8 * (4 * ks + cq)) : (u32x4){0u, 0u, 0u, 0u};
+            for (int ks = 0; ks < KS; ++ks) kf[pt][ks] = ok ? kf[pt][ks] : (u32x4){0u, 0u, 0u, 0u};
         }
         bf16x8 pf[MQ];
 #pragma unroll
@@ -356,18 +370,24 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
             for (int nb = 0; nb < NBD; ++nb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) o[mt][nb][i] *= corr;
-            uint16_t ph[8];
+            float pv[8];
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float x = st[pt][i];
-                    const float pv = x == -INFINITY ? 0.f : exp2f(x - mn);
-                    lsum[mt] += pv;
-                    ph[pt * 4 + i] = f32_to_bf16(pv);
+                    pv[pt * 4 + i] = x == -INFINITY ? 0.f : exp2f(x - mn);
+                    lsum[mt] += pv[pt * 4 + i];
                 }
-            pf[mt] = __builtin_bit_cast(bf16x8, (u32x4){ph[0] | ((uint32_t)ph[1] << 16), ph[2] | ((uint32_t)ph[3] << 16),
-                                                        ph[4] | ((uint32_t)ph[5] << 16), ph[6] | ((uint32_t)ph[7] << 16)});
+            pf[mt] = __builtin_bit_cast(bf16x8, (u32x4){pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                                                        pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])});
+        }
+        // V block -> wave-private LDS tile (row-major, padded)
+#pragma unroll
+        for (int t = 0; t < CPP / 2; ++t) {
+            const int piece = t * 64 + lane;
+            const int pos = piece / CPP, ch = piece - pos * CPP;
+            *(u32x4*)(vs + pos * LDV + ch * 8) = (blk + pos < wq1) ? vv[t] : (u32x4){0u, 0u, 0u, 0u};
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();

@@ -17,7 +17,9 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "_build", "libsdrl.so")
+# SDRL_LIB may name another build of the same library (e.g. one compiled with
+# different tile constants); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("SDRL_LIB") or os.path.join(HERE, "_build", "libsdrl.so")
 
 SD_OK, SD_E_INVAL, SD_E_NOMEM, SD_E_HIP, SD_E_STATE, SD_E_UNSUPPORTED = range(6)
 SD_DTYPE_F32, SD_DTYPE_BF16 = 0, 1
