@@ -333,8 +333,10 @@ extern "C" sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, v
 // ------------------------------------------------------------------ forward
 static act_t act_of(sd_engine e, bool draft) { return e->f32 ? ACT_F32 : (draft ? ACT_F16 : ACT_BF16); }
 
-static void proj(sd_engine e, bool draft, int layer, int which, const void* A, float* C, int M, int ldc,
-                 gemm_mode mode, hipStream_t s)
+// Returns the K splits of a deferred split-K projection (partials in gpart),
+// or 1 when C holds the result.
+static int proj(sd_engine e, bool draft, int layer, int which, const void* A, float* C, int M, int ldc, gemm_mode mode,
+                hipStream_t s)
 {
     int N, K;
     prj_shape(e->c, which, &N, &K);
@@ -342,48 +344,52 @@ static void proj(sd_engine e, bool draft, int layer, int which, const void* A, f
     if (draft) {
         const uint32_t* q = e->qw[4 * layer + which];
         const uint16_t* sc = e->qs[4 * layer + which];
-        if (e->f32) launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s);
-        else launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
-    } else {
-        const void* w = W(e, layer, widx[which]);
-        if (e->f32) launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s);
-        else launch_gemm_stream(1, (const uint16_t*)A, w, nullptr, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
+        if (e->f32) { launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s); return 1; }
+        return launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
     }
+    const void* w = W(e, layer, widx[which]);
+    if (e->f32) { launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s); return 1; }
+    return launch_gemm_stream(1, (const uint16_t*)A, w, nullptr, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
 }
 
 // One forward pass over B sequences x n tokens (row r = b*n + i at position
 // kv_len + off + i).  Token of row (b, i): i == 0 ? tokA[b*sA] :
-// tokB[b*sB + i - 1].  If logits != NULL, row r's logits go to logits + r*ldl.
+// tokB[b*sB + i - 1].  If logits != NULL, row r's logits go to logits + r*ldl;
+// otherwise the last layer's FFN (which only feeds the logits) is skipped.
 static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const int32_t* tokA, int sA,
                     const int32_t* tokB, int sB, int n, int off, float* logits, long ldl, hipStream_t s)
 {
     const sd_model_cfg& c = e->c;
     rows_t r = {B, n, off, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
     cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, c.n_kv, c.head_dim};
-    int R = B * n;
-    act_t at = act_of(e, draft);
-    int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
-    int pcls = draft ? T_Q4 : T_PROJ;
-    { tscope t(e, T_MISC, s); launch_embed(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, s); }
+    const int R = B * n;
+    const act_t at = act_of(e, draft);
+    const int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
+    const int pcls = draft ? T_Q4 : T_PROJ;
+    int S;
+    { tscope t(e, T_MISC, s);
+      launch_embed_rmsnorm(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, W(e, 0, 0), c.rms_eps, e->a, at, s); }
     for (int l = 0; l < c.n_layers; ++l) {
-        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, W(e, l, 0), e->f32, c.rms_eps, e->a, at, s); }
-        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s); }
-        { tscope t(e, T_MISC, s); launch_rope_kv(r, e->qkv, e->rope, c.n_q, kv, l, e->qrot, s); }
+        { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s); }
+        { tscope t(e, T_MISC, s); launch_rope_kv(r, e->qkv, e->gpart, S, e->rope, c.n_q, kv, l, e->qrot, s); }
+        if (!logits && l == c.n_layers - 1) break;      // the rest of the last layer only feeds the logits
         { tscope t(e, T_ATTN, s); launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s); }
-        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
-        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }
-        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s); }
-        { tscope t(e, T_MISC, s); launch_silu_mul(e->gu, R, c.ffn, e->act, at, s); }
-        { tscope t(e, pcls, s); proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s); }
+        { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
+        { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }
+        { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s); }
+        { tscope t(e, T_MISC, s); launch_silu_mul(e->gu, e->gpart, S, R, c.ffn, e->act, at, s); }
+        { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s); }
+        // next layer's attention norm, or the final norm (the LM head stays in the target precision)
+        const bool last = l == c.n_layers - 1;
+        const act_t nt = last ? (e->f32 ? ACT_F32 : ACT_BF16) : at;
+        const void* g = last ? e->w[1] : W(e, l + 1, 0);
+        { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, g, e->f32, c.rms_eps, e->a, nt, s); }
     }
     if (logits) {
-        // the LM head stays in the target precision for the drafter too
-        act_t lt = e->f32 ? ACT_F32 : ACT_BF16;
-        { tscope t(e, T_MISC, s); launch_rmsnorm(e->h, R, c.hidden, e->w[1], e->f32, c.rms_eps, e->a, lt, s); }
         tscope t(e, T_LMHEAD, s);
         if (e->f32) launch_gemm_f32((const float*)e->a, (const float*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
         else launch_gemm_stream(1, (const uint16_t*)e->a, e->w[2], nullptr, logits, e->gpart, e->gpart_cap, R, c.vocab,
-                                c.hidden, (int)ldl, GEMM_STORE, s);
+                                c.hidden, (int)ldl, GEMM_STORE, false, s);
     }
 }
 

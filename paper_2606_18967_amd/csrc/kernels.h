@@ -27,17 +27,21 @@ struct cache_t {
 };
 
 // ---- model kernels (kernels_model.hip)
-void launch_embed(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB,
-                  const void* E, int e_f32, int H, int V, float* h, hipStream_t s);
-void launch_rmsnorm(const float* h, int R, int H, const void* gain, int g_f32, float eps,
-                    void* out, act_t out_t, hipStream_t s);
-void launch_rope_kv(const rows_t& r, const float* qkv, const float2* rope, int n_q,
+// A kernel input produced by a split-K projection is given as partials P with
+// S > 1 splits ([S][rows][cols], summed on read); S <= 1 means the producer
+// wrote its output directly.
+void launch_embed_rmsnorm(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB,
+                          const void* E, int w_f32, int H, int V, float* h, const void* gain, float eps,
+                          void* out, act_t out_t, hipStream_t s);
+void launch_add_rmsnorm(float* h, const float* P, int S, int R, int H, const void* gain, int g_f32,
+                        float eps, void* out, act_t out_t, hipStream_t s);
+void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, const float2* rope, int n_q,
                     const cache_t& c, int layer, float* q_out, hipStream_t s);
 void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer,
                       float* part, int max_chunks, void* out, act_t out_t, hipStream_t s);
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks);
 int attention_chunk();
-void launch_silu_mul(const float* gu, int R, int F, void* out, act_t out_t, hipStream_t s);
+void launch_silu_mul(const float* gu, const float* P, int S, int R, int F, void* out, act_t out_t, hipStream_t s);
 void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const,
                        int32_t* kv_len, int max_slots, uint32_t* err, hipStream_t s);
 void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int span,
@@ -48,8 +52,12 @@ enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
 // Weight-streaming MFMA GEMM: wf 0 = int4 packed weights (Wt, scales Sc) with
 // fp16 activations, wf 1 = bf16 weights and activations.  part is split-K
 // scratch of part_cap floats (no split when too small).
-void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
-                        size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+// Returns the number of K splits S used.  With defer_reduce and S > 1 the
+// partials are left in part ([S][M][N]) for the consumer to sum; otherwise C
+// holds the result.
+int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
+                       size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, bool defer_reduce,
+                       hipStream_t s);
 size_t gemm_part_floats(int M, int N, int K);
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
                      gemm_mode mode, hipStream_t s);

@@ -475,8 +475,8 @@ static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const
     }
 }
 
-void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
-                        size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s)
+int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
+                       size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s)
 {
     if (use_tiled(wf, M, N, K)) {
         int mtw, S;
@@ -487,11 +487,11 @@ void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_
         dim3 grid((total + 7) / 8 * 8);
         const uint16_t* W = (const uint16_t*)Wt;
         k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
-        if (S > 1) {
+        if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
         }
-        return;
+        return S;
     }
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
@@ -508,10 +508,11 @@ void launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_
         if (nbw == 2) stream_mt<1, 2>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
         else stream_mt<1, 1>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
     }
-    if (S > 1) {
+    if (S > 1 && !defer_reduce) {
         size_t MN = (size_t)M * N;
         k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
     }
+    return S;
 }
 
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, gemm_mode mode,

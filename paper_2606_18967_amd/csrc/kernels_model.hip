@@ -24,36 +24,76 @@ template <> __device__ __forceinline__ void store_act<float>(void* out, size_t i
 template <> __device__ __forceinline__ void store_act<uint16_t>(void* out, size_t idx, float v) { ((uint16_t*)out)[idx] = f32_to_bf16(v); }
 template <> __device__ __forceinline__ void store_act<_Float16>(void* out, size_t idx, float v) { ((_Float16*)out)[idx] = (_Float16)v; }
 
-// ------------------------------------------------------------------ embed
-template <typename T>
-__global__ void __launch_bounds__(256) k_embed(rows_t r, const int32_t* tokA, int sA, const int32_t* tokB,
-                                               int sB, const T* E, int H, int V, float* h)
-{
-    int row = blockIdx.x;
-    int b = row / r.n, i = row - b * r.n;
-    int tok = (i == 0) ? tokA[(size_t)b * sA] : tokB[(size_t)b * sB + i - 1];
-    float* hr = h + (size_t)row * H;
-    if (tok < 0 || tok >= V) {
-        if (threadIdx.x == 0) flag_error(r.err, ERR_TOKEN);
-        for (int k = threadIdx.x; k < H; k += blockDim.x) hr[k] = 0.f;
-        return;
-    }
-    const T* er = E + (size_t)tok * H;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) hr[k] = elem<T>::load(er, k);
-}
+// ------------------------------------------------------------------ embed + rmsnorm
+// Inputs that come out of a split-K projection are read as the sum of the
+// partial products P[s][row][col] (s < S, S > 1); with S <= 1 the producer
+// wrote its output directly.
 
-// ------------------------------------------------------------------ rmsnorm
-template <typename G, typename O>
-__global__ void __launch_bounds__(256) k_rmsnorm(const float* h, int H, const G* gain, float eps, void* out)
+// h[row] = E[token(row)];  out[row] = RMSNorm(h[row]) * gain
+template <typename T, typename O>
+__global__ void __launch_bounds__(256) k_embed_rmsnorm(rows_t r, const int32_t* tokA, int sA, const int32_t* tokB,
+                                                       int sB, const T* E, int H, int V, float* h, const T* gain,
+                                                       float eps, void* out)
 {
     __shared__ float red[16];
-    const float* hr = h + (size_t)blockIdx.x * H;
+    const int row = blockIdx.x;
+    const int b = row / r.n, i = row - b * r.n;
+    const int tok = (i == 0) ? tokA[(size_t)b * sA] : tokB[(size_t)b * sB + i - 1];
+    const bool ok = tok >= 0 && tok < V;
+    if (!ok && threadIdx.x == 0) flag_error(r.err, ERR_TOKEN);
+    const T* er = E + (size_t)(ok ? tok : 0) * H;
+    float* hr = h + (size_t)row * H;
     float ss = 0.f;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) { float v = hr[k]; ss += v * v; }
+    for (int k = threadIdx.x; k < H; k += blockDim.x) {
+        const float x = ok ? elem<T>::load(er, k) : 0.f;
+        hr[k] = x;
+        ss += x * x;
+    }
     ss = block_sum(ss, red);
-    float inv = rsqrtf(ss / (float)H + eps);
+    const float inv = rsqrtf(ss / (float)H + eps);
     for (int k = threadIdx.x; k < H; k += blockDim.x)
-        store_act<O>(out, (size_t)blockIdx.x * H + k, hr[k] * inv * elem<G>::load(gain, k));
+        store_act<O>(out, (size_t)row * H + k, hr[k] * inv * elem<T>::load(gain, k));
+}
+
+// h[row] += sum_s P[s][row] (S > 1);  out[row] = RMSNorm(h[row]) * gain
+template <typename G, typename O>
+__global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, int S, int R, int H, const G* gain,
+                                                     float eps, void* out)
+{
+    __shared__ float red[16];
+    const int row = blockIdx.x;
+    float* hr = h + (size_t)row * H;
+    const size_t RH = (size_t)R * H;
+    float ss = 0.f;
+    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
+        float4 x = *(const float4*)(hr + k4);
+        if (S > 1) {
+            for (int sp = 0; sp < S; ++sp) {
+                const float4 p = *(const float4*)(P + sp * RH + (size_t)row * H + k4);
+                x.x += p.x; x.y += p.y; x.z += p.z; x.w += p.w;
+            }
+            *(float4*)(hr + k4) = x;
+        }
+        ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+    }
+    ss = block_sum(ss, red);
+    const float inv = rsqrtf(ss / (float)H + eps);
+    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
+        const float4 x = *(const float4*)(hr + k4);
+        const size_t o = (size_t)row * H + k4;
+        store_act<O>(out, o, x.x * inv * elem<G>::load(gain, k4));
+        store_act<O>(out, o + 1, x.y * inv * elem<G>::load(gain, k4 + 1));
+        store_act<O>(out, o + 2, x.z * inv * elem<G>::load(gain, k4 + 2));
+        store_act<O>(out, o + 3, x.w * inv * elem<G>::load(gain, k4 + 3));
+    }
+}
+
+__device__ __forceinline__ float sum_parts(const float* src, const float* P, int S, size_t RN, size_t idx)
+{
+    if (S <= 1) return src[idx];
+    float v = 0.f;
+    for (int sp = 0; sp < S; ++sp) v += P[sp * RN + idx];
+    return v;
 }
 
 // ------------------------------------------------------------------ rope + kv write
@@ -61,14 +101,16 @@ __global__ void __launch_bounds__(256) k_rmsnorm(const float* h, int H, const G*
 // the (cos, sin) table rope[pos][d/2].  q_out gets the rotated queries (fp32);
 // the rotated keys and the values go to the cache at the row's position.
 template <typename T>
-__global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, const float2* rope, int n_q,
-                                                 int n_kv, int d, T* kc, T* vc, int layer, float* q_out)
+__global__ void __launch_bounds__(1024) k_rope_kv(rows_t r, const float* qkv, const float* P, int S, const float2* rope,
+                                                 int n_q, int n_kv, int d, T* kc, T* vc, int layer, float* q_out)
 {
     int row = blockIdx.x;
     int b, i, slot, pos;
     bool ok = row_geom(r, row, &b, &i, &slot, &pos);
     int hd = d / 2;
-    const float* src = qkv + (size_t)row * (n_q + 2 * n_kv) * d;
+    const size_t RN = (size_t)r.B * r.n * (n_q + 2 * n_kv) * d;
+    const size_t base_idx = (size_t)row * (n_q + 2 * n_kv) * d;
+    auto src = [&](int c) { return sum_parts(qkv, P, S, RN, base_idx + c); };
     float* qo = q_out + (size_t)row * n_q * d;
     if (!ok) {
         if (threadIdx.x == 0) {
@@ -81,17 +123,16 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
     const float2* rp = rope + (size_t)pos * hd;
     for (int t = threadIdx.x; t < n_q * hd; t += blockDim.x) {
         int h = t / hd, k = t - h * hd;
-        float a = src[h * d + k], c = src[h * d + k + hd];
+        float a = src(h * d + k), c = src(h * d + k + hd);
         float2 cs = rp[k];
         qo[h * d + k] = a * cs.x - c * cs.y;
         qo[h * d + k + hd] = a * cs.y + c * cs.x;
     }
-    const float* ks = src + n_q * d;
-    const float* vs = ks + n_kv * d;
+    const int ko = n_q * d, vo = ko + n_kv * d;
     size_t base = (((size_t)layer * r.max_slots + slot) * n_kv) * (size_t)r.max_ctx;
     for (int t = threadIdx.x; t < n_kv * hd; t += blockDim.x) {
         int h = t / hd, k = t - h * hd;
-        float a = ks[h * d + k], c = ks[h * d + k + hd];
+        float a = src(ko + h * d + k), c = src(ko + h * d + k + hd);
         float2 cs = rp[k];
         size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
         elem<T>::store(kc, o + k, a * cs.x - c * cs.y);
@@ -100,7 +141,7 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
     for (int t = threadIdx.x; t < n_kv * d; t += blockDim.x) {
         int h = t / d, k = t - h * d;
         size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
-        elem<T>::store(vc, o + k, vs[t]);
+        elem<T>::store(vc, o + k, src(vo + t));
     }
 }
 
@@ -475,15 +516,33 @@ __global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int 
 }
 
 // ------------------------------------------------------------------ swiglu
+// out[row][f] = SiLU(g) * u with (g, u) = gu[row][f], gu[row][F + f]
 template <typename O>
-__global__ void __launch_bounds__(256) k_silu_mul(const float* gu, int F, void* out)
+__global__ void __launch_bounds__(256) k_silu_mul(const float* gu, const float* P, int S, int R, int F, void* out)
 {
-    const float* g = gu + (size_t)blockIdx.x * 2 * F;
-    const float* u = g + F;
-    for (int k = threadIdx.x; k < F; k += blockDim.x) {
-        float x = g[k];
-        store_act<O>(out, (size_t)blockIdx.x * F + k, x / (1.f + __expf(-x)) * u[k]);
+    const int row = blockIdx.x;
+    const int f = (blockIdx.y * 256 + threadIdx.x) * 4;
+    if (f >= F) return;
+    const size_t RN = (size_t)R * 2 * F;
+    const size_t gi = (size_t)row * 2 * F + f, ui = gi + F;
+    float4 g, u;
+    if (S <= 1) {
+        g = *(const float4*)(gu + gi);
+        u = *(const float4*)(gu + ui);
+    } else {
+        g = make_float4(0.f, 0.f, 0.f, 0.f);
+        u = g;
+        for (int sp = 0; sp < S; ++sp) {
+            const float4 a = *(const float4*)(P + sp * RN + gi), c = *(const float4*)(P + sp * RN + ui);
+            g.x += a.x; g.y += a.y; g.z += a.z; g.w += a.w;
+            u.x += c.x; u.y += c.y; u.z += c.z; u.w += c.w;
+        }
     }
+    const size_t o = (size_t)row * F + f;
+    store_act<O>(out, o, g.x / (1.f + __expf(-g.x)) * u.x);
+    store_act<O>(out, o + 1, g.y / (1.f + __expf(-g.y)) * u.y);
+    store_act<O>(out, o + 2, g.z / (1.f + __expf(-g.z)) * u.z);
+    store_act<O>(out, o + 3, g.w / (1.f + __expf(-g.w)) * u.w);
 }
 
 // ------------------------------------------------------------------ kv length
@@ -522,38 +581,52 @@ __global__ void k_kv_poison(const int32_t* slots, const int32_t* kv_len, int spa
 }  // namespace
 
 // ======================================================================= launchers
-void launch_embed(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB,
-                  const void* E, int e_f32, int H, int V, float* h, hipStream_t s)
+template <typename T>
+static void embed_norm_t(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB, const T* E, int H,
+                         int V, float* h, const T* gain, float eps, void* out, act_t t, hipStream_t s)
 {
-    int R = r.B * r.n;
-    if (e_f32) k_embed<float><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, (const float*)E, H, V, h);
-    else k_embed<uint16_t><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, (const uint16_t*)E, H, V, h);
+    const int R = r.B * r.n;
+    if (t == ACT_F32) k_embed_rmsnorm<T, float><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+    else if (t == ACT_BF16) k_embed_rmsnorm<T, uint16_t><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+    else k_embed_rmsnorm<T, _Float16><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+}
+
+void launch_embed_rmsnorm(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB, const void* E,
+                          int w_f32, int H, int V, float* h, const void* gain, float eps, void* out, act_t out_t,
+                          hipStream_t s)
+{
+    if (w_f32) embed_norm_t(r, tokA, sA, tokB, sB, (const float*)E, H, V, h, (const float*)gain, eps, out, out_t, s);
+    else embed_norm_t(r, tokA, sA, tokB, sB, (const uint16_t*)E, H, V, h, (const uint16_t*)gain, eps, out, out_t, s);
 }
 
 template <typename G>
-static void rmsnorm_t(const float* h, int R, int H, const G* g, float eps, void* out, act_t t, hipStream_t s)
+static void add_rmsnorm_t(float* h, const float* P, int S, int R, int H, const G* g, float eps, void* out, act_t t,
+                          hipStream_t s)
 {
-    if (t == ACT_F32) k_rmsnorm<G, float><<<R, 256, 0, s>>>(h, H, g, eps, out);
-    else if (t == ACT_BF16) k_rmsnorm<G, uint16_t><<<R, 256, 0, s>>>(h, H, g, eps, out);
-    else k_rmsnorm<G, _Float16><<<R, 256, 0, s>>>(h, H, g, eps, out);
+    const int th = H >= 4096 ? 1024 : 256;
+    if (t == ACT_F32) k_add_rmsnorm<G, float><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+    else if (t == ACT_BF16) k_add_rmsnorm<G, uint16_t><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+    else k_add_rmsnorm<G, _Float16><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
 }
 
-void launch_rmsnorm(const float* h, int R, int H, const void* gain, int g_f32, float eps, void* out,
-                    act_t out_t, hipStream_t s)
+void launch_add_rmsnorm(float* h, const float* P, int S, int R, int H, const void* gain, int g_f32, float eps,
+                        void* out, act_t out_t, hipStream_t s)
 {
-    if (g_f32) rmsnorm_t(h, R, H, (const float*)gain, eps, out, out_t, s);
-    else rmsnorm_t(h, R, H, (const uint16_t*)gain, eps, out, out_t, s);
+    if (g_f32) add_rmsnorm_t(h, P, S, R, H, (const float*)gain, eps, out, out_t, s);
+    else add_rmsnorm_t(h, P, S, R, H, (const uint16_t*)gain, eps, out, out_t, s);
 }
 
-void launch_rope_kv(const rows_t& r, const float* qkv, const float2* rope, int n_q, const cache_t& c,
-                    int layer, float* q_out, hipStream_t s)
+void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, const float2* rope, int n_q,
+                    const cache_t& c, int layer, float* q_out, hipStream_t s)
 {
     int R = r.B * r.n;
+    const int th = S > 1 ? 1024 : 256;
     if (c.kv_f32)
-        k_rope_kv<float><<<R, 256, 0, s>>>(r, qkv, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v, layer, q_out);
+        k_rope_kv<float><<<R, th, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v, layer,
+                                          q_out);
     else
-        k_rope_kv<uint16_t><<<R, 256, 0, s>>>(r, qkv, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
-                                              (uint16_t*)c.v, layer, q_out);
+        k_rope_kv<uint16_t><<<R, th, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
+                                             (uint16_t*)c.v, layer, q_out);
 }
 
 int attention_chunk() { return ATT_CH < MCH ? ATT_CH : MCH; }
@@ -607,11 +680,12 @@ void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c
     }
 }
 
-void launch_silu_mul(const float* gu, int R, int F, void* out, act_t out_t, hipStream_t s)
+void launch_silu_mul(const float* gu, const float* P, int S, int R, int F, void* out, act_t out_t, hipStream_t s)
 {
-    if (out_t == ACT_F32) k_silu_mul<float><<<R, 256, 0, s>>>(gu, F, out);
-    else if (out_t == ACT_BF16) k_silu_mul<uint16_t><<<R, 256, 0, s>>>(gu, F, out);
-    else k_silu_mul<_Float16><<<R, 256, 0, s>>>(gu, F, out);
+    dim3 grid(R, (F / 4 + 255) / 256);
+    if (out_t == ACT_F32) k_silu_mul<float><<<grid, 256, 0, s>>>(gu, P, S, R, F, out);
+    else if (out_t == ACT_BF16) k_silu_mul<uint16_t><<<grid, 256, 0, s>>>(gu, P, S, R, F, out);
+    else k_silu_mul<_Float16><<<grid, 256, 0, s>>>(gu, P, S, R, F, out);
 }
 
 void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const, int32_t* kv_len,
