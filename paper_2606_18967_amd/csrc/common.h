@@ -41,6 +41,17 @@ template <> struct elem<uint16_t> {
     static __device__ __forceinline__ void store(uint16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
 };
 
+// ------------------------------------------------------------ barriers
+// Work-group barrier that orders LDS only.  __syncthreads() also fences
+// global memory, which on this target waits for every outstanding global
+// load (vmcnt counts loads and stores) and so drains a kernel's prefetch.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // ------------------------------------------------------------ reductions
 __device__ __forceinline__ float wave_sum(float v)
 {

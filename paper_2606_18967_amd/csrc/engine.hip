@@ -77,6 +77,7 @@ struct sd_engine_s {
     uint32_t* err = nullptr;
     float* gpart = nullptr;      // split-K partial sums
     size_t gpart_cap = 0;        // floats
+    int launch_err = 0;          // a GEMM shape the kernels refused (reported by sd_sync)
     // kernel timing (diagnostics)
     bool timing = false;
     std::vector<hipEvent_t> ev_pool;
@@ -150,6 +151,8 @@ static sd_status check_cfg(const sd_model_cfg* c)
     if (((c->n_q + 2 * c->n_kv) * c->head_dim) % 64 || c->vocab % 64)
         return fail(SD_E_UNSUPPORTED, "(n_q+2*n_kv)*head_dim and vocab must be multiples of 64");
     if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return fail(SD_E_INVAL, "rms_eps and rope_theta must be > 0");
+    if (!gemm_q4_k_ok(c->hidden) || !gemm_q4_k_ok(c->ffn) || !gemm_q4_k_ok(c->n_q * c->head_dim))
+        return fail(SD_E_UNSUPPORTED, "hidden, ffn and n_q*head_dim must be 128*g*2^s with g <= 32, s <= 3");
     return SD_OK;
 }
 
@@ -345,7 +348,9 @@ static int proj(sd_engine e, bool draft, int layer, int which, const void* A, fl
         const uint32_t* q = e->qw[4 * layer + which];
         const uint16_t* sc = e->qs[4 * layer + which];
         if (e->f32) { launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s); return 1; }
-        return launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
+        const int S = launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
+        if (S < 1) e->launch_err = 1;   // cannot happen for a configuration check_cfg accepted
+        return S < 1 ? 1 : S;
     }
     const void* w = W(e, layer, widx[which]);
     if (e->f32) { launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s); return 1; }
@@ -523,6 +528,7 @@ extern "C" sd_status sd_sync(sd_engine e, void* stream)
     if (flags[ERR_SLOT]) return fail(SD_E_INVAL, "device: slot index outside [0, max_slots)");
     if (flags[ERR_TOKEN]) return fail(SD_E_INVAL, "device: token id outside [0, vocab)");
     if (flags[ERR_CTX]) return fail(SD_E_INVAL, "device: position at or beyond max_ctx");
+    if (e->launch_err) { e->launch_err = 0; return fail(SD_E_UNSUPPORTED, "an int4 GEMM shape was refused"); }
     return SD_OK;
 }
 

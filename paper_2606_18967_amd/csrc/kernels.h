@@ -59,6 +59,9 @@ int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t
                        size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, bool defer_reduce,
                        hipStream_t s);
 size_t gemm_part_floats(int M, int N, int K);
+// 1 if the int4 GEMM supports reduction length K (its splits stage at most 32
+// quantization groups of scales in LDS).
+int gemm_q4_k_ok(int K);
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
                      gemm_mode mode, hipStream_t s);
 void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,

@@ -38,7 +38,7 @@ __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, c
             As[kk][row] = gm < M ? A[(size_t)gm * K + k0 + kk] : 0.f;
             Ws[kk][row] = W[(size_t)(n0 + row) * K + k0 + kk];
         }
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int kk = 0; kk < FK; ++kk) {
             float a[4], b[4];
@@ -49,7 +49,7 @@ __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, c
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
         }
-        __syncthreads();
+        lds_barrier();
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -101,6 +101,7 @@ __device__ __forceinline__ float f16_bits_to_f32(uint16_t h) { return (float)__b
 constexpr int SK = 128;          // k per chunk (= one quantization group)
 constexpr int ALD = SK + 8;      // LDS row stride in 2-byte elements
 constexpr int SM = 64;           // rows per m-tile
+constexpr int SMAX_G = 32;       // most 128-k groups one int4 split may cover (scales staged in LDS)
 
 template <int WF, int NBW, int MT>
 __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict__ A, const void* __restrict__ Wt,
@@ -112,6 +113,10 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     constexpr int RD = WF == 0 ? 4 : 3;
     constexpr int WV = WF == 0 ? 1 : 4;                     // 16-byte vectors per lane per block per chunk
     __shared__ __attribute__((aligned(16))) uint16_t As[2][SM * ALD];
+    // int4 scales of this work-group's columns over its whole K range, staged
+    // once (loading them per chunk lets the compiler sink the loads to their
+    // use and wait on them there)
+    __shared__ __attribute__((aligned(16))) uint16_t Ss[WF == 0 ? 4 * NBW * SMAX_G * 16 : 8];
     const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     if (w >= total) return;
@@ -122,39 +127,55 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     const int G = K / SK, Gs = G / S, g0 = s * Gs, g1 = g0 + Gs;
     const int nb0 = (tile * 4 + wv) * NBW;
     const int rows = min(M - m0, MT * 16);                  // rows staged (others stay zero)
+    // scales: block b of the work-group (wave b / NBW, block b % NBW) has Gs*16
+    // contiguous fp16 scales, read as 16-byte vectors before the ring's loads
+    // so that waiting for them does not wait for the ring
+    constexpr int SV = WF == 0 ? (4 * NBW * SMAX_G * 2 + 255) / 256 : 1;
+    u32x4 sv[SV];
+    if constexpr (WF == 0) {
+#pragma unroll
+        for (int t = 0; t < SV; ++t) {
+            const int idx = min(tid + 256 * t, 4 * NBW * Gs * 2 - 1);
+            const int b = idx / (Gs * 2), r = idx - b * (Gs * 2);
+            sv[t] = *(const u32x4*)(Sc + ((size_t)(tile * 4 * NBW + b) * G + g0) * 16 + r * 8);
+        }
+    }
 
-    u32x4 a_reg[4];
-    auto load_a = [&](int g) {
+    // A tiles travel through a ring of register sets too (same depth as the
+    // weights): the tile of chunk c + 1 is requested RD - 2 chunks before it
+    // is stored to LDS
+    u32x4 ar[RD][4];
+    auto load_a = [&](int g, u32x4 (&a)[4]) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int pidx = tid + t * 256;
             const int row = pidx >> 4, col = (pidx & 15) * 8;
-            a_reg[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)g * SK + col);
+            a[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)g * SK + col);
         }
     };
-    auto store_a = [&](int buf) {
+    // a tile of a chunk past the split (valid false) is stored as zeros, so
+    // the padded iterations of the main loop add nothing
+    auto store_a = [&](int buf, const u32x4 (&a)[4], bool valid) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int pidx = tid + t * 256;
             const int row = pidx >> 4, col = (pidx & 15) * 8;
-            if (row < MT * 16) *(u32x4*)(&As[buf][row * ALD + col]) = row < rows ? a_reg[t] : (u32x4){0u, 0u, 0u, 0u};
+            if (row < MT * 16)
+                *(u32x4*)(&As[buf][row * ALD + col]) = (valid && row < rows) ? a[t] : (u32x4){0u, 0u, 0u, 0u};
         }
     };
     u32x4 wr[RD][NBW][WV];
-    uint16_t sr[RD][NBW];
-    auto load_w = [&](int g, u32x4 (&wq)[NBW][WV], uint16_t (&sq)[NBW]) {
+    auto load_w = [&](int g, u32x4 (&wq)[NBW][WV]) {
 #pragma unroll
         for (int i = 0; i < NBW; ++i) {
             const int nb = nb0 + i;
             if constexpr (WF == 0) {
                 wq[i][0] = ((const u32x4*)Wt)[((size_t)nb * G + g) * 64 + lane];
-                sq[i] = Sc[((size_t)nb * G + g) * 16 + (lane & 15)];
             } else {
                 const uint16_t* wp = (const uint16_t*)Wt + (size_t)(nb * 16 + (lane & 15)) * K + (size_t)g * SK +
                                      32 * (lane >> 4);
 #pragma unroll
                 for (int j = 0; j < WV; ++j) wq[i][j] = *(const u32x4*)(wp + 8 * j);
-                sq[i] = 0;
             }
         }
     };
@@ -165,7 +186,7 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
 #pragma unroll
         for (int t = 0; t < MT; ++t) acc[i][t] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
-    auto compute = [&](int buf, const u32x4 (&wq)[NBW][WV], const uint16_t (&sq)[NBW]) {
+    auto compute = [&](int buf, int g, const u32x4 (&wq)[NBW][WV]) {
         floatx4 tmp[NBW][MT];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -195,7 +216,8 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
         if constexpr (WF == 0) {
 #pragma unroll
             for (int i = 0; i < NBW; ++i) {
-                const float sc = f16_bits_to_f32(sq[i]);
+                // padded chunks (g >= g1) reuse the last staged scale: their A tile is zero
+                const float sc = f16_bits_to_f32(Ss[(wv * NBW + i) * SMAX_G * 16 + min(g - g0, Gs - 1) * 16 + (lane & 15)]);
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
 #pragma unroll
@@ -204,29 +226,45 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
         }
     };
 
-    // prologue: A of chunk g0 into LDS, weights of the first RD - 1 chunks in flight
-    load_a(g0);
+    // prologue: A and weights of the first RD - 1 chunks in flight, A of chunk g0 in LDS
+    // (chunk indices past the split are clamped: those loads are redundant but
+    // unconditional, which keeps the compiler's wait counts exact)
 #pragma unroll
-    for (int u = 0; u < RD - 1; ++u)
-        if (g0 + u < g1) load_w(g0 + u, wr[u], sr[u]);
-    store_a(0);
-    __syncthreads();
+    for (int u = 0; u < RD - 1; ++u) {
+        load_a(min(g0 + u, g1 - 1), ar[u]);
+        load_w(min(g0 + u, g1 - 1), wr[u]);
+    }
+    if constexpr (WF == 0) {
+#pragma unroll
+        for (int t = 0; t < SV; ++t) {
+            const int idx = tid + 256 * t;
+            if (idx < 4 * NBW * Gs * 2) {
+                const int b = idx / (Gs * 2), r = idx - b * (Gs * 2);
+                *(u32x4*)(&Ss[b * SMAX_G * 16 + r * 8]) = sv[t];
+            }
+        }
+    }
+    store_a(0, ar[0], true);
+    lds_barrier();
 
-    // chunk c uses ring slot (c - g0) % RD; at chunk c the A tile of c + 1 and
-    // the weights of c + RD - 1 are requested (A first, so waiting for it
-    // leaves the newer weight loads in flight)
-    for (int gb = g0; gb < g1; gb += RD) {
+    // chunk c uses ring slot u = (c - g0) % RD and LDS buffer (c - g0) & 1; it
+    // requests chunk c + RD - 1 (A before weights, so waiting for an A tile
+    // leaves the newer loads in flight) and stores the A tile of c + 1.  The
+    // chunk count is rounded up to a multiple of RD so the unrolled body has
+    // no branches: a conditional chunk would make the compiler's wait counts
+    // conservative at the merge and drain the whole ring every chunk.
+    const int gend = g0 + (Gs + RD - 1) / RD * RD;
+    for (int gb = g0; gb < gend; gb += RD) {
 #pragma unroll
         for (int u = 0; u < RD; ++u) {
             const int c = gb + u;
-            if (c < g1) {
-                const int buf = (c - g0) & 1;
-                if (c + 1 < g1) load_a(c + 1);
-                if (c + RD - 1 < g1) load_w(c + RD - 1, wr[(u + RD - 1) % RD], sr[(u + RD - 1) % RD]);
-                compute(buf, wr[u], sr[u]);
-                if (c + 1 < g1) store_a(buf ^ 1);
-                __syncthreads();
-            }
+            const int buf = (gb - g0 + u) & 1;
+            const int nx = (u + RD - 1) % RD;
+            load_a(min(c + RD - 1, g1 - 1), ar[nx]);
+            load_w(min(c + RD - 1, g1 - 1), wr[nx]);
+            compute(buf, c, wr[u]);
+            store_a(buf ^ 1, ar[(u + 1) % RD], c + 1 < g1);
+            lds_barrier();
         }
     }
 
@@ -315,7 +353,7 @@ __global__ void __launch_bounds__(256) k_gemm_tiled(const uint16_t* __restrict__
     load(k0, ra[0], rw[0]);
     if (k0 + 1 < k1) load(k0 + 1, ra[1], rw[1]);
     store(0, ra[0], rw[0]);
-    __syncthreads();
+    lds_barrier();
     for (int kb = k0; kb < k1; kb += 2) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
@@ -342,7 +380,7 @@ __global__ void __launch_bounds__(256) k_gemm_tiled(const uint16_t* __restrict__
                                                                                acc[i][j], 0, 0, 0);
                 }
                 if (k + 1 < k1) store(buf ^ 1, ra[u ^ 1], rw[u ^ 1]);
-                __syncthreads();
+                lds_barrier();
             }
         }
     }
@@ -426,9 +464,18 @@ void gemm_plan(int M, int N, int K, int* nbw, int* S)
     int msup = (M + SM - 1) / SM;
     int G = K / SK;
     int s = 1;
-    while (tiles * s * msup < GEMM_SPLIT_TARGET && G % (2 * s) == 0 && G / (2 * s) >= 2 && 2 * s <= GEMM_MAX_SPLIT)
+    while ((tiles * s * msup < GEMM_SPLIT_TARGET || G / s > SMAX_G) && G % (2 * s) == 0 && G / (2 * s) >= 2 &&
+           2 * s <= GEMM_MAX_SPLIT)
         s *= 2;
     *S = s;
+}
+
+int gemm_q4_k_ok(int K)
+{
+    if (K % SK) return 0;
+    int G = K / SK, s = 1;
+    while (G / s > SMAX_G && G % (2 * s) == 0 && 2 * s <= GEMM_MAX_SPLIT) s *= 2;
+    return G / s <= SMAX_G;
 }
 
 // bf16 GEMMs with more than 64 rows use the tiled kernel (N % 128 == 0).
@@ -496,6 +543,7 @@ int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
     if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
+    if (wf == 0 && K / SK / S > SMAX_G) return -1;      // the scales of one split must fit in LDS
     int msup = (M + SM - 1) / SM;
     int MT = msup > 1 ? 4 : (M + 15) / 16;
     int tiles = N / (64 * nbw);
