@@ -36,9 +36,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--ar-steps", type=int, default=20)
-    ap.add_argument("--cpu-seqs", type=int, default=2, help="sequences in the oracle's CPU sample")
+    ap.add_argument("--cpu-seqs", type=int, default=12, help="sequences in the oracle's CPU sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="write profiles/traffic.json from rocprofv3 --pmc outputs")
     return ap.parse_args()
 
 
@@ -47,10 +51,21 @@ def log(args, *a):
         print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_sources_hash():
+# source files each timing class's kernel is built from (a change to any of
+# them voids the committed counter readings for that class)
+SOURCES_OF_CLASS = {
+    "attn_decode": ("common.h", "kernels.h", "kernels_model.hip"),
+    "attn_verify": ("common.h", "kernels.h", "kernels_model.hip"),
+    "int4_proj": ("common.h", "kernels.h", "kernels_gemm.hip"),
+    "bf16_proj": ("common.h", "kernels.h", "kernels_gemm.hip"),
+    "lm_head": ("common.h", "kernels.h", "kernels_gemm.hip"),
+}
+
+
+def kernel_sources_hash(files=None):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_18967_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted(files or os.listdir(csrc)):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -58,20 +73,132 @@ def kernel_sources_hash():
 
 def measured_traffic(kind: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, or None if
-    the kernels changed since they were taken."""
+    the kernel's sources changed since they were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
             rec = json.load(fh)
     except (OSError, ValueError):
         return None
-    if rec.get("sources") != kernel_sources_hash():
+    d = rec.get("detail", {}).get(kind)
+    if not d or d.get("sources") != kernel_sources_hash(SOURCES_OF_CLASS[kind]):
         return None
-    return rec.get("per_launch_bytes", {}).get(kind)
+    return d.get("bytes")
+
+
+# the kernel each timing class brackets (bf16 KV cache, head_dim 128, M = 64 drafter rows)
+KERNEL_OF_CLASS = {
+    "attn_decode": "k_attn_mfma<128, 1>",
+    "attn_verify": "k_attn_mfma<128, 2>",
+    "int4_proj": "k_gemm_stream<0, 2, 4>",
+    "bf16_proj": "k_gemm_tiled<4>",
+    "lm_head": "k_gemm_stream<1, 2, 4> (draft rows), k_gemm_tiled<4> (verify rows)",
+}
+
+
+def algorithmic_per_launch(cfg, B, gamma, ctx):
+    """Bytes (HBM-bound classes) or FLOPs (MFMA-bound) one launch of each
+    timing class must move or do, for a mean cached length ctx (kv_len at the
+    start of the step): the sizes of what the operation reads and writes, not
+    what the kernels happen to transfer."""
+    H, V, d, nkv, nq, F = (cfg[x] for x in ("hidden", "vocab", "head_dim", "n_kv", "n_q", "ffn"))
+    kv_pos = nkv * d * 2 * 2                 # K and V bytes per cached position per layer (bf16)
+    q_row = nq * d * 4                       # fp32 rotated queries per token
+    # draft j (1..gamma) attends kv_len + j positions; verify attends kv_len + gamma + 1 once for all rows
+    attn_d = B * kv_pos * (ctx + (gamma + 1) / 2) + B * q_row
+    attn_v = B * kv_pos * (ctx + gamma + 1) + B * (gamma + 1) * q_row
+    w_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F          # projection weights per layer
+    q4 = (w_layer * 0.5 + w_layer / 128 * 2) / 4                         # mean int4 launch (4 per layer)
+    rows_v = B * (gamma + 1)
+    proj_flops = 2 * rows_v * w_layer / 4                                 # mean verify projection launch
+    lm = V * H * 2 + (gamma * B + rows_v) / (gamma + 1) * (H * 2 + V * 4)
+    return {"attn_decode": ("hbm", attn_d), "attn_verify": ("hbm", attn_v), "int4_proj": ("hbm", q4),
+            "bf16_proj": ("mfma", proj_flops), "lm_head": ("hbm", lm)}
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration(reps: int = 8):
+    """A plain device-to-device copy of COPY_BYTES (torch's copy kernel), for
+    scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": COPY_BYTES, "launches": reps}), flush=True)
+
+
+def kernel_key(name):
+    """'(anonymous namespace)::k_foo<128, 1>(args...)' -> 'k_foo<128,1>'."""
+    i = name.find("(anonymous namespace)::")
+    if i >= 0:
+        name = name[i + len("(anonymous namespace)::"):]
+    name = name.removeprefix("void ")
+    out, depth = [], 0
+    for ch in name:
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out).replace(" ", "")
+
+
+def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, out_path):
+    """Writes profiles/traffic.json from rocprofv3 --pmc counter_collection.csv
+    files: the bench run's FETCH_SIZE and WRITE_SIZE (KiB per dispatch)
+    averaged per kernel, scaled by what the same counters read for the
+    COPY_BYTES copy (the kernel with the largest reading in the copy runs)."""
+    import csv
+
+    def per_kernel(path, counter):
+        acc = {}
+        with open(path) as fh:
+            for row in csv.DictReader(fh):
+                if row.get("Counter_Name") != counter:
+                    continue
+                k = kernel_key(row["Kernel_Name"])
+                d = row.get("Dispatch_Id") or row.get("Correlation_Id")
+                acc.setdefault(k, {})
+                acc[k][d] = acc[k].get(d, 0.0) + float(row["Counter_Value"])
+        return {k: (sum(v.values()) / len(v), len(v)) for k, v in acc.items()}
+
+    def copy_factor(path, counter):
+        name, (kib, _) = max(per_kernel(path, counter).items(), key=lambda kv: kv[1][0])
+        return COPY_BYTES / (kib * 1024.0), name, kib
+
+    ff, fname, fkib = copy_factor(copy_fetch_csv, "FETCH_SIZE")
+    wf, wname, wkib = copy_factor(copy_write_csv, "WRITE_SIZE")
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    per = {}
+    for cls, kname in KERNEL_OF_CLASS.items():
+        k = kernel_key(kname)
+        if k not in fetch or k not in write:
+            continue
+        per[cls] = dict(kernel=k, fetch_bytes=fetch[k][0] * 1024 * ff, write_bytes=write[k][0] * 1024 * wf,
+                        bytes=fetch[k][0] * 1024 * ff + write[k][0] * 1024 * wf, dispatches=fetch[k][1],
+                        sources=kernel_sources_hash(SOURCES_OF_CLASS[cls]))
+    rec = {
+           "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib": fkib, "write_kib": wkib, "fetch_factor": ff,
+                                "write_factor": wf, "kernel": fname},
+           "per_launch_bytes": {c: v["bytes"] for c, v in per.items()}, "detail": per}
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec["per_launch_bytes"]))
 
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.ingest_pmc:
+        ingest_pmc(*args.ingest_pmc, os.path.join(ROOT, "profiles", "traffic.json"))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each GPU would run its own "
               "sequences independently; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
@@ -180,27 +307,18 @@ def main():
 
     # ---- roofline of the dominant kernel class
     H, V, d, nkv, nq, F, L = (cfg[x] for x in ("hidden", "vocab", "head_dim", "n_kv", "n_q", "ffn", "n_layers"))
-    ctx_prof = 0.5 * (kv_before + kv_after)             # mean context during the profiled steps
+    ctx_prof = 0.5 * (kv_before + kv_after)             # mean kv_len at the start of the profiled steps
     dom = max(classes, key=lambda c: classes[c]["ms_per_step"])
-    # algorithmic bytes per launch ("Measurement")
-    R_d, R_v = B, B * (gamma + 1)
-    la = (gamma * L, L)  # attention launches: per draft forward and per verify
-    kv_row = nkv * d * 2 * 2                          # K and V bytes per cached position (bf16)
-    attn_bytes = B * kv_row * (ctx_prof + (gamma + 1) / 2) + (R_d * gamma + R_v) / sum(la) * (nq * d * 4 + nq * d * 2)
-    q4_w = (H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F)     # weights per layer
-    q4_bytes = (q4_w * 0.5 + q4_w / 128 * 2) / 4               # mean per projection launch (4 per layer)
-    lm_bytes = V * H * 2 + (gamma * R_d + R_v) / (gamma + 1) * (H * 2 + V * 4)
-    proj_flops = 2 * R_v * q4_w / 4
-    algo = {"attention": ("hbm", attn_bytes), "int4_proj": ("hbm", q4_bytes), "lm_head": ("hbm", lm_bytes),
-            "bf16_proj": ("mfma", proj_flops)}
+    algo = algorithmic_per_launch(cfg, B, gamma, ctx_prof)
     bound, amount = algo.get(dom, ("hbm", float("nan")))
     us = classes[dom]["us_per_launch"]
     if bound == "hbm":
         achieved, peak, unit = amount / (us * 1e-6) / 1e9, HBM_PEAK_GBS, "GB/s"
     else:
         achieved, peak, unit = amount / (us * 1e-6) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
-    roof = dict(kernel=dom, bound=bound, achieved=round(achieved, 1), peak=peak, unit=unit,
+    roof = dict(bound=bound, achieved=round(achieved, 1), peak=peak, unit=unit,
                 frac=round(achieved / peak, 4), traffic=measured_traffic(dom),
+                kernel=KERNEL_OF_CLASS.get(dom, dom), timing_class=dom,
                 algorithmic_per_launch=amount, us_per_launch=round(us, 2))
     others = {}
     for name, (b, amt) in algo.items():

@@ -188,10 +188,12 @@ sd_status sd_set_debug(sd_engine e, int32_t poison);
 
 /* Kernel timing (diagnostics).  While on, the engine brackets each launch of
  * a kernel class with HIP events recorded on the launch stream.  Classes:
- * 0 attention, 1 int4 projections (drafter), 2 bf16/fp32 projections
- * (target layers), 3 LM head, 4 token sampler, 5 accept, 6 norms / RoPE /
- * embedding / SwiGLU / KV bookkeeping.  sd_timing(e, 1) also clears the
- * accumulated records. */
+ * 0 attention over the cache for one query token per sequence (draft and AR
+ * steps; the partial kernel only), 1 attention for the gamma+1 verify
+ * queries (partial kernel), 2 int4 projections (drafter), 3 bf16/fp32
+ * projections (target layers), 4 LM head, 5 token sampler, 6 accept,
+ * 7 norms / RoPE / embedding / SwiGLU / attention combine / KV bookkeeping.
+ * sd_timing(e, 1) also clears the accumulated records. */
 sd_status sd_timing(sd_engine e, int32_t on);
 
 /* Waits for the recorded events and returns, for class `cls`, the summed

@@ -637,10 +637,9 @@ size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
 }
 
 template <typename T, int D>
-static void attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                   int max_chunks, void* out, act_t out_t, hipStream_t s)
+static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
+                         int max_chunks, hipStream_t s)
 {
-    int chunk = ATT_CH;
     if constexpr (sizeof(T) == 2) {
         // bf16 cache: MFMA kernel, chunks of MCH positions (max_chunks counts ATT_CH chunks, ATT_CH <= MCH)
         const int QR = (n_q / c.n_kv) * r.n;
@@ -656,28 +655,32 @@ static void attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, i
             case 3: k_attn_mfma<D, 3><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
             default: k_attn_mfma<D, 4><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
         }
-        max_chunks = mch;
-        chunk = MCH;
+        return attn_split{mch, MCH};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
         k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
+        return attn_split{max_chunks, ATT_CH};
     }
-    int R = r.B * r.n;
-    if (out_t == ACT_F32) k_attn_combine<float><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
-    else if (out_t == ACT_BF16) k_attn_combine<uint16_t><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
-    else k_attn_combine<_Float16><<<R * n_q, D, 0, s>>>(r, n_q, D, part, max_chunks, chunk, out);
 }
 
-void launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                      int max_chunks, void* out, act_t out_t, hipStream_t s)
+attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
+                            int max_chunks, hipStream_t s)
 {
     if (c.head_dim == 128) {
-        if (c.kv_f32) attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
-        else attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
-    } else {
-        if (c.kv_f32) attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
-        else attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, s);
+        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, s);
     }
+    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, s);
+    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, s);
+}
+
+void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
+                              act_t out_t, hipStream_t s)
+{
+    const int R = r.B * r.n, D = head_dim;
+    if (out_t == ACT_F32) k_attn_combine<float><<<R * n_q, D, 0, s>>>(r, n_q, D, part, sp.chunks, sp.chunk, out);
+    else if (out_t == ACT_BF16) k_attn_combine<uint16_t><<<R * n_q, D, 0, s>>>(r, n_q, D, part, sp.chunks, sp.chunk, out);
+    else k_attn_combine<_Float16><<<R * n_q, D, 0, s>>>(r, n_q, D, part, sp.chunks, sp.chunk, out);
 }
 
 void launch_silu_mul(const float* gu, const float* P, int S, int R, int F, void* out, act_t out_t, hipStream_t s)

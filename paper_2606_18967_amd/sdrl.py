@@ -35,7 +35,7 @@ API_SYMBOLS = (
 
 # kernel classes of sd_timing_read
 T_ATTN, T_Q4, T_PROJ, T_LMHEAD, T_SAMPLE, T_ACCEPT, T_MISC = range(7)
-T_NAMES = ("attention", "int4_proj", "bf16_proj", "lm_head", "sampler", "accept", "misc")
+T_NAMES = ("attn_decode", "attn_verify", "int4_proj", "bf16_proj", "lm_head", "sampler", "accept", "misc")
 
 
 class SDError(RuntimeError):
