@@ -121,12 +121,13 @@ size_t sd_drafter_bytes(const sd_model_cfg* cfg);
  * layer of the bound target into qbuf (device, >= sd_drafter_bytes).
  * Embedding, norms and LM head are shared with the target, unquantized.
  * Per group of 128 weights of one row: s = fp16(max|w|/7),
- * q = clamp(rint(w/s), -8, 7).  Packed layout per matrix [N][K]: for
- * n-block nb = n/16 and group g = k/128, 64 lanes x 4 uint32 words; lane
- * l = n%16 + 16*c holds in word j the 8 codes k = 128g + 32j + 8c + e,
- * code e in the nibble at bit 4*(e/2) + 16*(e%2), stored as q + 8; word
- * index ((nb*G + g)*64 + l)*4 + j with G = K/128; scale index
- * (nb*G + g)*16 + n%16.  Must be called again after the weights change. */
+ * q = clamp(rint(w/s), -8, 7).  Packed layout per matrix [N][K] (N a
+ * multiple of 32, G = K/128): for column block nb = n/32 and group
+ * g = k/128, 512 uint32 words; lane l = n%32 + 32*h (h = 0, 1) holds for
+ * k-step st = 0..7 the word with the 8 codes k = 128g + 16st + 8h + e,
+ * code e in the nibble at bit 4*(e/2) + 16*(e%2), stored as q + 8, at word
+ * index (((nb*G + g)*2 + st/4)*64 + l)*4 + st%4; scale index
+ * (nb*G + g)*32 + n%32.  Must be called again after the weights change. */
 sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream);
 
 /* --------------------------------------------------------- the SD step */

@@ -82,22 +82,24 @@ def compare_ar(x_oracle: int, gap: float, p_oracle, x_dev: int, p_dev, tol: floa
 
 def unpack_q4(packed: np.ndarray, scales_bits: np.ndarray, N: int, K: int):
     """Codes [N][K] (int8) and scales [N][K/128] (fp16 bits) from the
-    library's packed tile layout (documented in include/sd_api.h)."""
+    library's packed layout (documented in include/sd_api.h): for column
+    block nb = n/32 and group g, word (((nb*G + g)*2 + st//4)*64 + l)*4 + st%4
+    of lane l = n%32 + 32*h holds codes k = 128g + 16st + 8h + e at nibble
+    4*(e//2) + 16*(e%2), stored as q + 8; scale (nb*G + g)*32 + n%32."""
     G = K // 128
-    words = packed.view(np.uint32).reshape(N // 16, G, 64, 4)
+    words = packed.view(np.uint32).reshape(N // 32, G, 2, 64, 4)     # [nb, g, st//4, lane, st%4]
     codes = np.zeros((N, K), dtype=np.int8)
-    l = np.arange(64)
-    n_in = l % 16
-    c = l // 16
-    for j in range(4):
-        w = words[:, :, :, j]                       # [nb, g, lane]
+    lanes = np.arange(64)
+    cols = (np.arange(N // 32)[:, None] * 32 + (lanes % 32)[None, :])  # [nb, lane]
+    h = lanes // 32
+    for st in range(8):
+        w = words[:, :, st // 4, :, st % 4]                             # [nb, g, lane]
         for e in range(8):
-            nib = (w >> np.uint32(4 * (e // 2) + 16 * (e % 2))) & np.uint32(15)
-            k_in = 32 * j + 8 * c + e               # per lane
+            nib = ((w >> np.uint32(4 * (e // 2) + 16 * (e % 2))) & np.uint32(15)).astype(np.int16) - 8
             for g in range(G):
-                rows = (np.arange(N // 16)[:, None] * 16 + n_in[None, :])
-                codes[rows, g * 128 + k_in[None, :]] = nib[:, g, :].astype(np.int16) - 8
-    sc = scales_bits.view(np.uint16).reshape(N // 16, G, 16).transpose(0, 2, 1).reshape(N, G)
+                ks = g * 128 + 16 * st + 8 * h + e                      # per lane
+                codes[cols, ks[None, :]] = nib[:, g, :]
+    sc = scales_bits.view(np.uint16).reshape(N // 32, G, 32).transpose(0, 2, 1).reshape(N, G)
     return codes, sc
 
 

@@ -185,11 +185,20 @@ static size_t gpart_bytes(const sd_model_cfg& c, int R)
             prj_shape(c, w, &N, &K);
             size_t f = gemm_part_floats(m, N, K);
             mx = f > mx ? f : mx;
+            f = gemm_q4_part_floats(m, N, K);
+            mx = f > mx ? f : mx;
         }
         size_t f = gemm_part_floats(m, c.vocab, c.hidden);
         mx = f > mx ? f : mx;
     }
-    { int m = R; for (int w = 0; w < 4; ++w) { int N, K; prj_shape(c, w, &N, &K); size_t f = gemm_part_floats(m, N, K); mx = f > mx ? f : mx; } }
+    for (int w = 0; w < 4; ++w) {
+        int N, K;
+        prj_shape(c, w, &N, &K);
+        size_t f = gemm_part_floats(R, N, K);
+        mx = f > mx ? f : mx;
+        f = gemm_q4_part_floats(R, N, K);
+        mx = f > mx ? f : mx;
+    }
     return (mx > 64 ? mx : 64) * 4;
 }
 
@@ -348,13 +357,13 @@ static int proj(sd_engine e, bool draft, int layer, int which, const void* A, fl
         const uint32_t* q = e->qw[4 * layer + which];
         const uint16_t* sc = e->qs[4 * layer + which];
         if (e->f32) { launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s); return 1; }
-        const int S = launch_gemm_stream(0, (const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
+        const int S = launch_gemm_q4((const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
         if (S < 1) e->launch_err = 1;   // cannot happen for a configuration check_cfg accepted
         return S < 1 ? 1 : S;
     }
     const void* w = W(e, layer, widx[which]);
     if (e->f32) { launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s); return 1; }
-    return launch_gemm_stream(1, (const uint16_t*)A, w, nullptr, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
+    return launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
 }
 
 // One forward pass over B sequences x n tokens (row r = b*n + i at position
@@ -395,7 +404,7 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
     if (logits) {
         tscope t(e, T_LMHEAD, s);
         if (e->f32) launch_gemm_f32((const float*)e->a, (const float*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
-        else launch_gemm_stream(1, (const uint16_t*)e->a, e->w[2], nullptr, logits, e->gpart, e->gpart_cap, R, c.vocab,
+        else launch_gemm_bf16((const uint16_t*)e->a, (const uint16_t*)e->w[2], logits, e->gpart, e->gpart_cap, R, c.vocab,
                                 c.hidden, (int)ldl, GEMM_STORE, false, s);
     }
 }

@@ -54,18 +54,22 @@ void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int sp
 
 // ---- GEMMs (kernels_gemm.hip): C[M][N] (fp32, row stride ldc) = or += A[M][K] W^T
 enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
-// Weight-streaming MFMA GEMM: wf 0 = int4 packed weights (Wt, scales Sc) with
-// fp16 activations, wf 1 = bf16 weights and activations.  part is split-K
-// scratch of part_cap floats (no split when too small).
-// Returns the number of K splits S used.  With defer_reduce and S > 1 the
-// partials are left in part ([S][M][N]) for the consumer to sum; otherwise C
-// holds the result.
-int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
-                       size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, bool defer_reduce,
-                       hipStream_t s);
+// bf16 MFMA GEMM: weight-streaming kernel for M <= 64 per m-tile, LDS-tiled
+// kernel for M > 64.  part is split-K scratch of part_cap floats (no split
+// when too small).  Returns the number of K splits S used.  With
+// defer_reduce and S > 1 the partials are left in part ([S][M][N]) for the
+// consumer to sum; otherwise C holds the result.
+int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part, size_t part_cap, int M, int N, int K,
+                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s);
 size_t gemm_part_floats(int M, int N, int K);
-// 1 if the int4 GEMM supports reduction length K (its splits stage at most 32
-// quantization groups of scales in LDS).
+// ---- int4 drafter GEMM (kernels_q4.hip): C[M][N] (+)= A[M][K] Wq^T, A fp16,
+// Wq in the packed 32-column tile layout, N % 32 == 0.  Returns the number of
+// K splits S (partials left in part as [S][M][N] when S > 1, for the consumer
+// to sum), or -1 for an unsupported shape or a too small part.
+int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, float* C, float* part, size_t part_cap,
+                   int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+size_t gemm_q4_part_floats(int M, int N, int K);
+// 1 if the int4 GEMM supports reduction length K.
 int gemm_q4_k_ok(int K);
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
                      gemm_mode mode, hipStream_t s);

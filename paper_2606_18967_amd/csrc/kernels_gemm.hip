@@ -1,19 +1,11 @@
-// kernels_gemm.hip -- the projections: C[M][N] (fp32) = or += A[M][K] W^T.
+// kernels_gemm.hip -- the bf16 projections: C[M][N] (fp32) = or += A[M][K] W^T.
 //
 // Weights are row-major [N][K] (K contiguous), activations [M][K].
-//   - gemm_stream (bf16 or int4 weights, MFMA): see k_gemm_stream.  int4
-//     group-128 weights in the packed tile layout written by the RTN quantizer
-//     are dequantized in registers to exact fp16 integers and fed to
-//     v_mfma_f32_16x16x32_f16; the per-group fp16 scale is applied to the fp32
-//     partial sum of each group.
-//   - gemm_f32 / gemm_q4_f32: plain VALU versions for fp32 models.
-//
-// Packed int4 layout (per weight matrix, N % 16 == 0, K % 128 == 0): for
-// n-block nb = n/16 and group g = k/128 there are 64 lanes x 4 words; lane
-// l = (n % 16) + 16*c holds, in word j, the 8 weights k = 128g + 32j + 8c + e
-// (e = 0..7) of row n, element e in the nibble at bit 4*(e/2) + 16*(e%2),
-// stored as code + 8.  Word address: ((nb*G + g)*64 + l)*4 + j.  Scales are
-// fp16 at ((nb*G + g)*16 + n%16).
+//   - gemm_stream (M <= 64 per m-tile): weights streamed from HBM into
+//     registers, v_mfma_f32_16x16x32_bf16; see k_gemm_stream.
+//   - gemm_tiled (M > 64, the verify forward): both operands through LDS.
+//   - gemm_f32 / gemm_q4_f32: plain VALU versions for fp32 models (the int4
+//     one reads the packed layout of kernels_q4.hip).
 #include "common.h"
 #include "kernels.h"
 
@@ -63,60 +55,33 @@ __global__ void __launch_bounds__(256) k_gemm_f32(const float* __restrict__ A, c
     }
 }
 
-// ------------------------------------------------------------------ int4 dequant helpers
-// One packed word -> 8 fp16 values equal to the signed codes (exact).
-__device__ __forceinline__ half8 dequant8(uint32_t x)
-{
-    const uint32_t MAGIC = 0x64006400u;       // fp16 1024.0 in both halves
-    uint32_t r0 = (x & 0x000F000Fu) | MAGIC;
-    uint32_t r1 = ((x >> 4) & 0x000F000Fu) | MAGIC;
-    uint32_t r2 = ((x >> 8) & 0x000F000Fu) | MAGIC;
-    uint32_t r3 = ((x >> 12) & 0x000F000Fu) | MAGIC;
-    const half2v bias = {(_Float16)1032.0f, (_Float16)1032.0f};   // 1024 + 8
-    half2v h0 = __builtin_bit_cast(half2v, r0) - bias;
-    half2v h1 = __builtin_bit_cast(half2v, r1) - bias;
-    half2v h2 = __builtin_bit_cast(half2v, r2) - bias;
-    half2v h3 = __builtin_bit_cast(half2v, r3) - bias;
-    half8 out = {h0[0], h0[1], h1[0], h1[1], h2[0], h2[1], h3[0], h3[1]};
-    return out;
-}
-
 __device__ __forceinline__ float f16_bits_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 
-// ------------------------------------------------------------------ weight-streaming MFMA GEMM
-// C[M][N] = A[M][K] W^T for decode-shaped M (a few to a few hundred rows).
-// A work-group covers a 64-row m-tile, 64*NBW columns (NBW 16-column blocks
-// per wave, 4 waves) and a range of K split into chunks of 128.  The A chunk
-// is staged in LDS (double-buffered) and shared by the four waves; each wave
-// streams its weight columns from HBM straight into registers one chunk
-// ahead of the MFMAs, so every weight byte is read once per m-tile.  With
-// several K splits the partial sums go to P[s][M][N] and k_splitk_reduce adds
-// them up.  Work items are laid out so that consecutive ones (the m-tiles of
-// one column tile) land on the same XCD and share its L2.
-//   WF = 0: int4 packed weights, fp16 activations (v_mfma_f32_16x16x32_f16);
-//           in chunk g, k-step j, lane l covers k = 128g + 32j + 8(l/16) + 0..7.
-//   WF = 1: bf16 weights and activations (v_mfma_f32_16x16x32_bf16); lane l
-//           covers k = 128g + 32(l/16) + 8j + 0..7 so that its 64 bytes of a
-//           weight row are contiguous.
-constexpr int SK = 128;          // k per chunk (= one quantization group)
+// ------------------------------------------------------------------ weight-streaming bf16 MFMA GEMM
+// C[M][N] = A[M][K] W^T for decode-shaped M (up to 64 rows per m-tile; the
+// AR step and the draft LM head).  A work-group covers a 64-row m-tile,
+// 64*NBW columns (NBW 16-column blocks per wave, 4 waves) and a range of K
+// split into chunks of 128.  The A chunk is staged in LDS (double-buffered)
+// and shared by the four waves; each wave streams its weight columns from
+// HBM straight into registers through a ring of RD register sets (RD - 1
+// chunks in flight), so every weight byte is read once per m-tile.  Lane l
+// covers k = 128g + 32(l/16) + 8j + 0..7 of chunk g in k-step j
+// (v_mfma_f32_16x16x32_bf16), so its 64 bytes of a weight row are
+// contiguous; A is read from LDS in the same k order.  With several K splits
+// the partial sums go to P[s][M][N] for the consumer (or k_splitk_reduce).
+// Work items are laid out so that consecutive ones (the m-tiles of one
+// column tile) land on the same XCD and share its L2.
+constexpr int SK = 128;          // k per chunk
 constexpr int ALD = SK + 8;      // LDS row stride in 2-byte elements
 constexpr int SM = 64;           // rows per m-tile
-constexpr int SMAX_G = 32;       // most 128-k groups one int4 split may cover (scales staged in LDS)
 
-template <int WF, int NBW, int MT>
-__global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict__ A, const void* __restrict__ Wt,
-                                                     const uint16_t* __restrict__ Sc, float* __restrict__ C,
-                                                     float* __restrict__ P, int M, int N, int K, int ldc, int mode,
-                                                     int S, int msup, int total)
+template <int NBW, int MT>
+__global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wt,
+                                                     float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
+                                                     int ldc, int mode, int S, int msup, int total)
 {
-    // weights are prefetched RD - 1 chunks ahead through a ring of register sets
-    constexpr int RD = WF == 0 ? 4 : 3;
-    constexpr int WV = WF == 0 ? 1 : 4;                     // 16-byte vectors per lane per block per chunk
+    constexpr int RD = 3;
     __shared__ __attribute__((aligned(16))) uint16_t As[2][SM * ALD];
-    // int4 scales of this work-group's columns over its whole K range, staged
-    // once (loading them per chunk lets the compiler sink the loads to their
-    // use and wait on them there)
-    __shared__ __attribute__((aligned(16))) uint16_t Ss[WF == 0 ? 4 * NBW * SMAX_G * 16 : 8];
     const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     if (w >= total) return;
@@ -127,19 +92,6 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     const int G = K / SK, Gs = G / S, g0 = s * Gs, g1 = g0 + Gs;
     const int nb0 = (tile * 4 + wv) * NBW;
     const int rows = min(M - m0, MT * 16);                  // rows staged (others stay zero)
-    // scales: block b of the work-group (wave b / NBW, block b % NBW) has Gs*16
-    // contiguous fp16 scales, read as 16-byte vectors before the ring's loads
-    // so that waiting for them does not wait for the ring
-    constexpr int SV = WF == 0 ? (4 * NBW * SMAX_G * 2 + 255) / 256 : 1;
-    u32x4 sv[SV];
-    if constexpr (WF == 0) {
-#pragma unroll
-        for (int t = 0; t < SV; ++t) {
-            const int idx = min(tid + 256 * t, 4 * NBW * Gs * 2 - 1);
-            const int b = idx / (Gs * 2), r = idx - b * (Gs * 2);
-            sv[t] = *(const u32x4*)(Sc + ((size_t)(tile * 4 * NBW + b) * G + g0) * 16 + r * 8);
-        }
-    }
 
     // A tiles travel through a ring of register sets too (same depth as the
     // weights): the tile of chunk c + 1 is requested RD - 2 chunks before it
@@ -164,19 +116,13 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
                 *(u32x4*)(&As[buf][row * ALD + col]) = (valid && row < rows) ? a[t] : (u32x4){0u, 0u, 0u, 0u};
         }
     };
-    u32x4 wr[RD][NBW][WV];
-    auto load_w = [&](int g, u32x4 (&wq)[NBW][WV]) {
+    u32x4 wr[RD][NBW][4];
+    auto load_w = [&](int g, u32x4 (&wq)[NBW][4]) {
 #pragma unroll
         for (int i = 0; i < NBW; ++i) {
-            const int nb = nb0 + i;
-            if constexpr (WF == 0) {
-                wq[i][0] = ((const u32x4*)Wt)[((size_t)nb * G + g) * 64 + lane];
-            } else {
-                const uint16_t* wp = (const uint16_t*)Wt + (size_t)(nb * 16 + (lane & 15)) * K + (size_t)g * SK +
-                                     32 * (lane >> 4);
+            const uint16_t* wp = Wt + (size_t)((nb0 + i) * 16 + (lane & 15)) * K + (size_t)g * SK + 32 * (lane >> 4);
 #pragma unroll
-                for (int j = 0; j < WV; ++j) wq[i][j] = *(const u32x4*)(wp + 8 * j);
-            }
+            for (int j = 0; j < 4; ++j) wq[i][j] = *(const u32x4*)(wp + 8 * j);
         }
     };
 
@@ -186,42 +132,20 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
 #pragma unroll
         for (int t = 0; t < MT; ++t) acc[i][t] = (floatx4){0.f, 0.f, 0.f, 0.f};
 
-    auto compute = [&](int buf, int g, const u32x4 (&wq)[NBW][WV]) {
-        floatx4 tmp[NBW][MT];
+    auto compute = [&](int buf, const u32x4 (&wq)[NBW][4]) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int acol = WF == 0 ? 32 * j + 8 * (lane >> 4) : 32 * (lane >> 4) + 8 * j;
-            const uint16_t* ab = &As[buf][(lane & 15) * ALD + acol];
+            const uint16_t* ab = &As[buf][(lane & 15) * ALD + 32 * (lane >> 4) + 8 * j];
             u32x4 af[MT];
 #pragma unroll
             for (int t = 0; t < MT; ++t) af[t] = *(const u32x4*)(ab + t * 16 * ALD);
 #pragma unroll
             for (int i = 0; i < NBW; ++i) {
-                if constexpr (WF == 0) {
-                    const half8 bq = dequant8(wq[i][0][j]);
-#pragma unroll
-                    for (int t = 0; t < MT; ++t)
-                        tmp[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            __builtin_bit_cast(half8, af[t]), bq, j == 0 ? (floatx4){0.f, 0.f, 0.f, 0.f} : tmp[i][t],
-                            0, 0, 0);
-                } else {
-                    const bf16x8 bb = __builtin_bit_cast(bf16x8, wq[i][j]);
-#pragma unroll
-                    for (int t = 0; t < MT; ++t)
-                        acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[t]), bb,
-                                                                           acc[i][t], 0, 0, 0);
-                }
-            }
-        }
-        if constexpr (WF == 0) {
-#pragma unroll
-            for (int i = 0; i < NBW; ++i) {
-                // padded chunks (g >= g1) reuse the last staged scale: their A tile is zero
-                const float sc = f16_bits_to_f32(Ss[(wv * NBW + i) * SMAX_G * 16 + min(g - g0, Gs - 1) * 16 + (lane & 15)]);
+                const bf16x8 bb = __builtin_bit_cast(bf16x8, wq[i][j]);
 #pragma unroll
                 for (int t = 0; t < MT; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[i][t][r] += sc * tmp[i][t][r];
+                    acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[t]), bb,
+                                                                       acc[i][t], 0, 0, 0);
             }
         }
     };
@@ -233,16 +157,6 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     for (int u = 0; u < RD - 1; ++u) {
         load_a(min(g0 + u, g1 - 1), ar[u]);
         load_w(min(g0 + u, g1 - 1), wr[u]);
-    }
-    if constexpr (WF == 0) {
-#pragma unroll
-        for (int t = 0; t < SV; ++t) {
-            const int idx = tid + 256 * t;
-            if (idx < 4 * NBW * Gs * 2) {
-                const int b = idx / (Gs * 2), r = idx - b * (Gs * 2);
-                *(u32x4*)(&Ss[b * SMAX_G * 16 + r * 8]) = sv[t];
-            }
-        }
     }
     store_a(0, ar[0], true);
     lds_barrier();
@@ -262,7 +176,7 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
             const int nx = (u + RD - 1) % RD;
             load_a(min(c + RD - 1, g1 - 1), ar[nx]);
             load_w(min(c + RD - 1, g1 - 1), wr[nx]);
-            compute(buf, c, wr[u]);
+            compute(buf, wr[u]);
             store_a(buf ^ 1, ar[(u + 1) % RD], c + 1 < g1);
             lds_barrier();
         }
@@ -418,12 +332,13 @@ __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__
 }
 
 // ------------------------------------------------------------------ int4 x fp32 VALU
+// code of weight (n, k) in the packed layout of kernels_q4.hip
 __device__ __forceinline__ int q4_code(const uint32_t* Wq, int G, int n, int k)
 {
-    int nb = n >> 4, g = k >> 7;
-    int l = (n & 15) + 16 * ((k & 31) >> 3);
-    int j = (k & 127) >> 5, e = k & 7;
-    uint32_t word = Wq[(((size_t)nb * G + g) * 64 + l) * 4 + j];
+    const int nb = n >> 5, g = k >> 7, kk = k & 127;
+    const int st = kk >> 4, h = (kk >> 3) & 1, e = kk & 7;
+    const int l = (n & 31) + 32 * h;
+    const uint32_t word = Wq[((((size_t)nb * G + g) * 2 + (st >> 2)) * 64 + l) * 4 + (st & 3)];
     return (int)((word >> (4 * (e >> 1) + 16 * (e & 1))) & 15u) - 8;
 }
 
@@ -440,7 +355,7 @@ __global__ void __launch_bounds__(256) k_gemm_q4_f32(const float* __restrict__ A
     for (int g = 0; g < G; ++g) {
         float part = 0.f;
         for (int k = g * 128; k < g * 128 + 128; ++k) part += ar[k] * (float)q4_code(Wq, G, n, k);
-        acc += f16_bits_to_f32(Sc[((size_t)(n >> 4) * G + g) * 16 + (n & 15)]) * part;
+        acc += f16_bits_to_f32(Sc[((size_t)(n >> 5) * G + g) * 32 + (n & 31)]) * part;
     }
     float* cp = C + (size_t)m * ldc + n;
     *cp = mode == GEMM_ADD ? *cp + acc : acc;
@@ -464,22 +379,13 @@ void gemm_plan(int M, int N, int K, int* nbw, int* S)
     int msup = (M + SM - 1) / SM;
     int G = K / SK;
     int s = 1;
-    while ((tiles * s * msup < GEMM_SPLIT_TARGET || G / s > SMAX_G) && G % (2 * s) == 0 && G / (2 * s) >= 2 &&
-           2 * s <= GEMM_MAX_SPLIT)
+    while (tiles * s * msup < GEMM_SPLIT_TARGET && G % (2 * s) == 0 && G / (2 * s) >= 2 && 2 * s <= GEMM_MAX_SPLIT)
         s *= 2;
     *S = s;
 }
 
-int gemm_q4_k_ok(int K)
-{
-    if (K % SK) return 0;
-    int G = K / SK, s = 1;
-    while (G / s > SMAX_G && G % (2 * s) == 0 && 2 * s <= GEMM_MAX_SPLIT) s *= 2;
-    return G / s <= SMAX_G;
-}
-
 // bf16 GEMMs with more than 64 rows use the tiled kernel (N % 128 == 0).
-static bool use_tiled(int wf, int M, int N, int K) { return wf == 1 && M > 64 && N % TBN == 0 && K % TBK == 0; }
+static bool use_tiled(int M, int N, int K) { return M > 64 && N % TBN == 0 && K % TBK == 0; }
 
 static int tiled_mtw(int M)
 {
@@ -502,7 +408,7 @@ size_t gemm_part_floats(int M, int N, int K)
 {
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
-    if (use_tiled(1, M, N, K)) {
+    if (use_tiled(M, N, K)) {
         int mtw, St;
         tiled_plan(M, N, K, &mtw, &St);
         S = St > S ? St : S;
@@ -510,29 +416,28 @@ size_t gemm_part_floats(int M, int N, int K)
     return S > 1 ? (size_t)S * M * N : 0;
 }
 
-template <int WF, int NBW>
-static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C,
-                      float* P, int M, int N, int K, int ldc, int mode, int S, int msup, int total)
+template <int NBW>
+static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const uint16_t* W, float* C, float* P, int M,
+                      int N, int K, int ldc, int mode, int S, int msup, int total)
 {
     switch (MT) {
-        case 1: k_gemm_stream<WF, NBW, 1><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        case 2: k_gemm_stream<WF, NBW, 2><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        case 3: k_gemm_stream<WF, NBW, 3><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        default: k_gemm_stream<WF, NBW, 4><<<grid, 256, 0, s>>>(A, Wt, Sc, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 1: k_gemm_stream<NBW, 1><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 2: k_gemm_stream<NBW, 2><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 3: k_gemm_stream<NBW, 3><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        default: k_gemm_stream<NBW, 4><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
     }
 }
 
-int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t* Sc, float* C, float* part,
-                       size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s)
+int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part, size_t part_cap, int M, int N, int K,
+                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s)
 {
-    if (use_tiled(wf, M, N, K)) {
+    if (use_tiled(M, N, K)) {
         int mtw, S;
         tiled_plan(M, N, K, &mtw, &S);
         if (S > 1 && (size_t)S * M * N > part_cap) S = 1;
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
-        const uint16_t* W = (const uint16_t*)Wt;
         k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
@@ -543,19 +448,13 @@ int launch_gemm_stream(int wf, const uint16_t* A, const void* Wt, const uint16_t
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
     if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
-    if (wf == 0 && K / SK / S > SMAX_G) return -1;      // the scales of one split must fit in LDS
     int msup = (M + SM - 1) / SM;
     int MT = msup > 1 ? 4 : (M + 15) / 16;
     int tiles = N / (64 * nbw);
     int total = tiles * S * msup;
     dim3 grid((total + 7) / 8 * 8);
-    if (wf == 0) {
-        if (nbw == 2) stream_mt<0, 2>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
-        else stream_mt<0, 1>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
-    } else {
-        if (nbw == 2) stream_mt<1, 2>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
-        else stream_mt<1, 1>(MT, grid, s, A, Wt, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
-    }
+    if (nbw == 2) stream_mt<2>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
+    else stream_mt<1>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
     if (S > 1 && !defer_reduce) {
         size_t MN = (size_t)M * N;
         k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
