@@ -8,6 +8,9 @@
 
 namespace {
 
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+
 __device__ __forceinline__ bool row_geom(const rows_t& r, int row, int* b, int* i, int* slot, int* pos)
 {
     *b = row / r.n;
@@ -97,51 +100,58 @@ __device__ __forceinline__ float sum_parts(const float* src, const float* P, int
 }
 
 // ------------------------------------------------------------------ rope + kv write
-// qkv row = [q (n_q*d) | k (n_kv*d) | v (n_kv*d)], fp32.  RoPE rotate-half with
-// the (cos, sin) table rope[pos][d/2].  q_out gets the rotated queries (fp32);
-// the rotated keys and the values go to the cache at the row's position.
+// qkv row = [q (n_q*d) | k (n_kv*d) | v (n_kv*d)], fp32: n_q + 2 n_kv head
+// units of d columns.  RoPE rotate-half with the (cos, sin) table
+// rope[pos][d/2].  q_out gets the rotated queries (fp32); the rotated keys and
+// the values go to the cache at the row's position.  Work-group (row, group
+// of upw head units); each thread takes one (unit, k) pair, columns k and
+// k + d/2 of the unit.
 template <typename T>
-__global__ void __launch_bounds__(1024) k_rope_kv(rows_t r, const float* qkv, const float* P, int S, const float2* rope,
-                                                 int n_q, int n_kv, int d, T* kc, T* vc, int layer, float* q_out)
+__global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, const float* P, int S, const float2* rope,
+                                                 int n_q, int n_kv, int d, T* kc, T* vc, int layer, float* q_out,
+                                                 int upw)
 {
-    int row = blockIdx.x;
+    const int row = blockIdx.x;
     int b, i, slot, pos;
-    bool ok = row_geom(r, row, &b, &i, &slot, &pos);
-    int hd = d / 2;
-    const size_t RN = (size_t)r.B * r.n * (n_q + 2 * n_kv) * d;
-    const size_t base_idx = (size_t)row * (n_q + 2 * n_kv) * d;
-    auto src = [&](int c) { return sum_parts(qkv, P, S, RN, base_idx + c); };
+    const bool ok = row_geom(r, row, &b, &i, &slot, &pos);
+    const int hd = d / 2, units = n_q + 2 * n_kv;
+    const int u0 = blockIdx.y * upw, nu = min(upw, units - u0);
+    const size_t RN = (size_t)r.B * r.n * units * d;
+    const size_t base_idx = (size_t)row * units * d;
     float* qo = q_out + (size_t)row * n_q * d;
     if (!ok) {
-        if (threadIdx.x == 0) {
-            bool bad_slot = slot < 0 || slot >= r.max_slots;
+        if (threadIdx.x == 0 && blockIdx.y == 0) {
+            const bool bad_slot = slot < 0 || slot >= r.max_slots;
             flag_error(r.err, bad_slot ? ERR_SLOT : ERR_CTX);
         }
-        for (int t = threadIdx.x; t < n_q * d; t += blockDim.x) qo[t] = 0.f;
+        for (int t = threadIdx.x; t < nu * d; t += blockDim.x) {
+            const int u = u0 + t / d;
+            if (u < n_q) qo[(size_t)u * d + t % d] = 0.f;
+        }
         return;
     }
     const float2* rp = rope + (size_t)pos * hd;
-    for (int t = threadIdx.x; t < n_q * hd; t += blockDim.x) {
-        int h = t / hd, k = t - h * hd;
-        float a = src(h * d + k), c = src(h * d + k + hd);
-        float2 cs = rp[k];
-        qo[h * d + k] = a * cs.x - c * cs.y;
-        qo[h * d + k + hd] = a * cs.y + c * cs.x;
-    }
-    const int ko = n_q * d, vo = ko + n_kv * d;
-    size_t base = (((size_t)layer * r.max_slots + slot) * n_kv) * (size_t)r.max_ctx;
-    for (int t = threadIdx.x; t < n_kv * hd; t += blockDim.x) {
-        int h = t / hd, k = t - h * hd;
-        float a = src(ko + h * d + k), c = src(ko + h * d + k + hd);
-        float2 cs = rp[k];
-        size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
-        elem<T>::store(kc, o + k, a * cs.x - c * cs.y);
-        elem<T>::store(kc, o + k + hd, a * cs.y + c * cs.x);
-    }
-    for (int t = threadIdx.x; t < n_kv * d; t += blockDim.x) {
-        int h = t / d, k = t - h * d;
-        size_t o = ((base + (size_t)h * r.max_ctx) + pos) * d;
-        elem<T>::store(vc, o + k, src(vo + t));
+    const size_t cbase = (((size_t)layer * r.max_slots + slot) * n_kv) * (size_t)r.max_ctx;
+    for (int t = threadIdx.x; t < nu * hd; t += blockDim.x) {
+        const int u = u0 + t / hd, k = t - (t / hd) * hd;
+        const size_t c0 = base_idx + (size_t)u * d + k;
+        const float a = sum_parts(qkv, P, S, RN, c0), c = sum_parts(qkv, P, S, RN, c0 + hd);
+        if (u < n_q + n_kv) {
+            const float2 cs = rp[k];
+            const float x0 = a * cs.x - c * cs.y, x1 = a * cs.y + c * cs.x;
+            if (u < n_q) {
+                qo[(size_t)u * d + k] = x0;
+                qo[(size_t)u * d + k + hd] = x1;
+            } else {
+                const size_t o = (cbase + (size_t)(u - n_q) * r.max_ctx + pos) * d;
+                elem<T>::store(kc, o + k, x0);
+                elem<T>::store(kc, o + k + hd, x1);
+            }
+        } else {
+            const size_t o = (cbase + (size_t)(u - n_q - n_kv) * r.max_ctx + pos) * d;
+            elem<T>::store(vc, o + k, a);
+            elem<T>::store(vc, o + k + hd, c);
+        }
     }
 }
 
@@ -267,9 +277,10 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
     }
 }
 
-// MFMA attention for a bf16 cache.  Work-group (b, kv head, chunk of MCH
-// positions, query-row slice z); each wave takes a quarter of the chunk in
-// blocks of 32 positions.  Per block:
+// MFMA attention for a bf16 cache.  Work-group (b, kv head, chunk, query-row
+// slice z): a sequence's context is split evenly into ceil(ctx / MCH) chunks
+// and each wave takes a quarter of its chunk in blocks of 32 positions.  Per
+// block:
 //   S^T = K Q^T with v_mfma_f32_16x16x32_bf16: K rows straight from global
 //   memory (lane l: position l%16 of a 16-row tile, dims 8*(4ks + l/16)+0..7),
 //   Q^T pre-scaled by log2(e)/sqrt(d).  Lane l then holds the scores of query
@@ -277,8 +288,11 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 //   is exactly the B operand layout of the next product, so P never leaves
 //   registers.
 //   O^T += V^T P^T: V is staged row-major in a wave-private LDS tile (row
-//   stride d + 8, bank-conflict free for the gather) and read transposed.
-// The online softmax runs per query row in base 2; the four waves are merged
+//   stride d + 8) and read back transposed with ds_read_b64_tr_b16.
+//   The next block's K and V are loaded while the current one computes.
+// The online softmax runs per query row in base 2 with lazy rescaling (the
+// reference max of a row moves only when the block max exceeds it by more
+// than 8, bounding the exp2 terms by 256); the four waves are merged
 // through LDS and the chunk result (m in natural-log units, l, o[d]) goes to
 // the same partial buffer k_attn_combine reads.
 #ifndef ATT_MFMA_CHUNK
@@ -286,8 +300,10 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 #endif
 constexpr int MCH = ATT_MFMA_CHUNK;   // positions per work-group
 
+// two waves per SIMD where the registers allow it without spills (one query
+// tile); the verify variants keep one
 template <int D, int MQ>
-__global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
+__global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
                                                    const uint16_t* vc, int layer, float* part, int max_chunks)
 {
     constexpr int KS = D / 32;      // k-steps over the head dim
@@ -299,15 +315,21 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
 
     const int b = blockIdx.x / n_kv, kvh = blockIdx.x - b * n_kv;
     const int c = blockIdx.y, z = blockIdx.z;
-    const int slot = r.slots[b];
+    // wave-uniform by construction; readfirstlane lets the compiler keep them
+    // (and the buffer resources built from them) in scalar registers
+    const int slot = __builtin_amdgcn_readfirstlane(r.slots[b]);
     if (slot < 0 || slot >= r.max_slots) return;   // flagged by k_rope_kv
-    const int basepos = r.kv_len[slot] + r.off;
+    const int basepos = __builtin_amdgcn_readfirstlane(r.kv_len[slot]) + r.off;
     int ctx = basepos + r.n;
     if (ctx > r.max_ctx) ctx = r.max_ctx;
-    const int p0 = c * MCH;
+    // the sequence's ceil(ctx / MCH) chunks (the count k_attn_combine reads)
+    // split its context evenly, in multiples of 32 positions
+    const int nch = (ctx + MCH - 1) / MCH;
+    const int clen = ((ctx + nch - 1) / nch + 31) & ~31;
+    const int p0 = c * clen;
     if (p0 >= ctx) return;
-    const int p1 = min(p0 + MCH, ctx);
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int p1 = min(p0 + clen, ctx);
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int cq = lane >> 4, lr = lane & 15;
     const int G = n_q / n_kv, QR = G * r.n;
     const int qbase = z * 16 * MQ;
@@ -354,30 +376,33 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
         for (int nb = 0; nb < NBD; ++nb) o[mt][nb] = (floatx4){0.f, 0.f, 0.f, 0.f};
     }
 
-    const int wq0 = p0 + w * (MCH / 4), wq1 = min(p0 + (w + 1) * (MCH / 4), p1);
-    for (int blk = wq0; blk < wq1; blk += 32) {
-        // K fragments for the two 16-position tiles, then the V block; positions
-        // past the wave's range read its last position and are zeroed
-        u32x4 kf[2][KS];
+    const int wlen = ((clen + 3) / 4 + 31) & ~31;                  // positions per wave
+    const int wq0 = p0 + w * wlen, wq1 = min(wq0 + wlen, p1);
+    // K fragments of the two 16-position tiles and the V block of the block at
+    // blk, through buffer resources limited to the cached positions: reads at
+    // or past ctx return 0 without touching memory.  Positions past the wave's
+    // range get -inf scores below, so their P is 0.
+    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, ctx * D * 2, 0x00020000);
+    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)V, 0, ctx * D * 2, 0x00020000);
+    const int koff = (lr * D + 8 * cq) * 2;                         // + (16 pt) D 2 + 64 ks
+    const int voff = ((lane / CPP) * D + (lane % CPP) * 8) * 2;     // + t (64 / CPP) D 2
+    auto load_kv = [&](int blk, u32x4 (&kf)[2][KS], u32x4 (&vv)[CPP / 2]) {
+        const int sb = __builtin_amdgcn_readfirstlane(blk * D * 2);   // scalar offset of the block
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt) {
-            const int pos = min(blk + 16 * pt + lr, wq1 - 1);
+        for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kf[pt][ks] = *(const u32x4*)(K + (size_t)pos * D + 8 * (4 * ks + cq));
-        }
-        u32x4 vv[CPP / 2];
+            for (int ks = 0; ks < KS; ++ks)
+                kf[pt][ks] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                           krs, koff + (16 * pt * D + 32 * ks) * 2, sb, 0));
 #pragma unroll
-        for (int t = 0; t < CPP / 2; ++t) {
-            const int piece = t * 64 + lane;
-            const int pos = piece / CPP, ch = piece - pos * CPP;
-            vv[t] = *(const u32x4*)(V + (size_t)min(blk + pos, wq1 - 1) * D + ch * 8);
-        }
-#pragma unroll
-        for (int pt = 0; pt < 2; ++pt) {
-            const bool ok = blk + 16 * pt + lr < wq1;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kf[pt][ks] = ok ? kf[pt][ks] : (u32x4){0u, 0u, 0u, 0u};
-        }
+        for (int t = 0; t < CPP / 2; ++t)
+            vv[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                  vrs, voff + t * (64 / CPP) * D * 2, sb, 0));
+    };
+    // lane l's pieces of the transposing LDS reads that build V^T fragments:
+    // positions 4*(l/16) + (l%16)/4 (+16), dims 4*(l%4) of each 16-dim block
+    const int trow = 4 * cq + (lr >> 2), tcol = 4 * (lr & 3);
+    auto block = [&](int blk, const u32x4 (&kf)[2][KS], const u32x4 (&vv)[CPP / 2]) {
         bf16x8 pf[MQ];
 #pragma unroll
         for (int mt = 0; mt < MQ; ++mt) {
@@ -403,14 +428,21 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
                 }
             bm = fmaxf(bm, __shfl_xor(bm, 16, WAVE));
             bm = fmaxf(bm, __shfl_xor(bm, 32, WAVE));
-            const float mn = fmaxf(m[mt], bm);
-            const float corr = m[mt] == -INFINITY ? 0.f : exp2f(m[mt] - mn);
-            m[mt] = mn;
-            lsum[mt] *= corr;
+            // lazy rescaling: a row moves its reference max (and rescales its
+            // sums) only when the block max exceeds it by more than 8, so the
+            // exp2 terms stay <= 256; the result is the same softmax
+            const bool need = bm > m[mt] + 8.f;
+            if (__builtin_amdgcn_ballot_w64(need)) {
+                const float mn = need ? bm : m[mt];
+                const float corr = m[mt] == -INFINITY ? 0.f : exp2f(m[mt] - mn);
+                m[mt] = mn;
+                lsum[mt] *= corr;
 #pragma unroll
-            for (int nb = 0; nb < NBD; ++nb)
+                for (int nb = 0; nb < NBD; ++nb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) o[mt][nb][i] *= corr;
+                    for (int i = 0; i < 4; ++i) o[mt][nb][i] *= corr;
+            }
+            const float mn = m[mt];
             float pv[8];
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt)
@@ -428,27 +460,38 @@ __global__ void __launch_bounds__(256) k_attn_mfma(rows_t r, const float* q, int
         for (int t = 0; t < CPP / 2; ++t) {
             const int piece = t * 64 + lane;
             const int pos = piece / CPP, ch = piece - pos * CPP;
-            *(u32x4*)(vs + pos * LDV + ch * 8) = (blk + pos < wq1) ? vv[t] : (u32x4){0u, 0u, 0u, 0u};
+            *(u32x4*)(vs + pos * LDV + ch * 8) = vv[t];
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // O^T += V^T P^T
+        // O^T += V^T P^T; V^T fragments from two transposing reads: lane l gets
+        // dim 16 nb + l%16 at positions 4(l/16) + 0..3 and 16 + 4(l/16) + 0..3,
+        // the k order of pf
 #pragma unroll
         for (int nb = 0; nb < NBD; ++nb) {
-            uint16_t vh[8];
-#pragma unroll
-            for (int pt = 0; pt < 2; ++pt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) vh[pt * 4 + i] = vs[(16 * pt + 4 * cq + i) * LDV + 16 * nb + lr];
-            const bf16x8 vt = __builtin_bit_cast(bf16x8, (u32x4){vh[0] | ((uint32_t)vh[1] << 16), vh[2] | ((uint32_t)vh[3] << 16),
-                                                                 vh[4] | ((uint32_t)vh[5] << 16), vh[6] | ((uint32_t)vh[7] << 16)});
+            const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4s*)(vs + trow * LDV + 16 * nb + tcol));
+            const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4s*)(vs + (16 + trow) * LDV + 16 * nb + tcol));
+            const bf16x8 vt = __builtin_bit_cast(bf16x8, (v8s){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
             for (int mt = 0; mt < MQ; ++mt) o[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pf[mt], o[mt][nb], 0, 0, 0);
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    // two register sets: the next block's K and V load while this one computes
+    u32x4 kf0[2][KS], kf1[2][KS], vv0[CPP / 2], vv1[CPP / 2];
+    load_kv(wq0, kf0, vv0);
+    for (int blk = wq0; blk < wq1; blk += 64) {
+        load_kv(blk + 32, kf1, vv1);
+        block(blk, kf0, vv0);
+        if (blk + 32 >= wq1) break;
+        load_kv(blk + 64, kf0, vv0);
+        block(blk + 32, kf1, vv1);
     }
 #pragma unroll
     for (int mt = 0; mt < MQ; ++mt) {
@@ -619,14 +662,15 @@ void launch_add_rmsnorm(float* h, const float* P, int S, int R, int H, const voi
 void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, const float2* rope, int n_q,
                     const cache_t& c, int layer, float* q_out, hipStream_t s)
 {
-    int R = r.B * r.n;
-    const int th = S > 1 ? 1024 : 256;
+    const int R = r.B * r.n, units = n_q + 2 * c.n_kv;
+    const int upw = 512 / c.head_dim;                       // head units per work-group: 256 threads, one pair each
+    dim3 grid(R, (units + upw - 1) / upw);
     if (c.kv_f32)
-        k_rope_kv<float><<<R, th, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v, layer,
-                                          q_out);
+        k_rope_kv<float><<<grid, 256, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v,
+                                              layer, q_out, upw);
     else
-        k_rope_kv<uint16_t><<<R, th, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
-                                             (uint16_t*)c.v, layer, q_out);
+        k_rope_kv<uint16_t><<<grid, 256, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
+                                                 (uint16_t*)c.v, layer, q_out, upw);
 }
 
 int attention_chunk() { return ATT_CH < MCH ? ATT_CH : MCH; }
