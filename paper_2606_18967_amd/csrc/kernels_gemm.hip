@@ -387,20 +387,23 @@ void gemm_plan(int M, int N, int K, int* nbw, int* S)
 // bf16 GEMMs with more than 64 rows use the tiled kernel (N % 128 == 0).
 static bool use_tiled(int M, int N, int K) { return M > 64 && N % TBN == 0 && K % TBK == 0; }
 
-static int tiled_mtw(int M)
-{
-    (void)M;
-    return 4;   // 128-row tiles: two work-groups per CU (the 160-row variant fits one)
-}
+// Tile height: 160 rows when they divide M and N is small enough that the
+// splits, not the row waste, decide the time (measured on the verify shapes
+// at M = 320: qkv, o and down projections); 128 rows otherwise.
+static int tiled_mtw(int M, int N) { return (M % 160 == 0 && N <= 8192) ? 5 : 4; }
+
+#ifndef TILED_SPLIT_TARGET
+#define TILED_SPLIT_TARGET 192
+#endif
 
 static void tiled_plan(int M, int N, int K, int* mtw, int* S)
 {
-    *mtw = tiled_mtw(M);
+    *mtw = tiled_mtw(M, N);
     int mtiles = (M + 32 * *mtw - 1) / (32 * *mtw);
     int tiles = N / TBN * mtiles;
     int KS = K / TBK;
     int s = 1;
-    while (tiles * s < GEMM_SPLIT_TARGET && KS % (2 * s) == 0 && KS / (2 * s) >= 4 && 2 * s <= GEMM_MAX_SPLIT) s *= 2;
+    while (tiles * s < TILED_SPLIT_TARGET && KS % (2 * s) == 0 && KS / (2 * s) >= 4 && 2 * s <= GEMM_MAX_SPLIT) s *= 2;
     *S = s;
 }
 
@@ -438,7 +441,8 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
-        k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
+        if (mtw == 5) k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
+        else k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);

@@ -27,16 +27,40 @@ template <> __device__ __forceinline__ void store_act<float>(void* out, size_t i
 template <> __device__ __forceinline__ void store_act<uint16_t>(void* out, size_t idx, float v) { ((uint16_t*)out)[idx] = f32_to_bf16(v); }
 template <> __device__ __forceinline__ void store_act<_Float16>(void* out, size_t idx, float v) { ((_Float16*)out)[idx] = (_Float16)v; }
 
+// four consecutive outputs (idx % 4 == 0) in one store
+template <typename T>
+__device__ __forceinline__ void store_act4(void* out, size_t idx, float4 v);
+template <> __device__ __forceinline__ void store_act4<float>(void* out, size_t idx, float4 v) { *(float4*)((float*)out + idx) = v; }
+template <> __device__ __forceinline__ void store_act4<uint16_t>(void* out, size_t idx, float4 v)
+{
+    *(uint2*)((uint16_t*)out + idx) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+}
+template <> __device__ __forceinline__ void store_act4<_Float16>(void* out, size_t idx, float4 v)
+{
+    const half2v a = {(_Float16)v.x, (_Float16)v.y}, b = {(_Float16)v.z, (_Float16)v.w};
+    *(uint2*)((_Float16*)out + idx) = make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+}
+
 // ------------------------------------------------------------------ embed + rmsnorm
 // Inputs that come out of a split-K projection are read as the sum of the
 // partial products P[s][row][col] (s < S, S > 1); with S <= 1 the producer
 // wrote its output directly.
 
+// four consecutive elements of a weight row as floats (H % 4 == 0)
+template <typename T> __device__ __forceinline__ float4 load4(const T* p);
+template <> __device__ __forceinline__ float4 load4<float>(const float* p) { return *(const float4*)p; }
+template <> __device__ __forceinline__ float4 load4<uint16_t>(const uint16_t* p)
+{
+    const uint2 v = *(const uint2*)p;
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+                       __uint_as_float(v.y & 0xffff0000u));
+}
+
 // h[row] = E[token(row)];  out[row] = RMSNorm(h[row]) * gain
 template <typename T, typename O>
-__global__ void __launch_bounds__(256) k_embed_rmsnorm(rows_t r, const int32_t* tokA, int sA, const int32_t* tokB,
-                                                       int sB, const T* E, int H, int V, float* h, const T* gain,
-                                                       float eps, void* out)
+__global__ void __launch_bounds__(1024) k_embed_rmsnorm(rows_t r, const int32_t* tokA, int sA, const int32_t* tokB,
+                                                        int sB, const T* E, int H, int V, float* h, const T* gain,
+                                                        float eps, void* out)
 {
     __shared__ float red[16];
     const int row = blockIdx.x;
@@ -47,15 +71,19 @@ __global__ void __launch_bounds__(256) k_embed_rmsnorm(rows_t r, const int32_t* 
     const T* er = E + (size_t)(ok ? tok : 0) * H;
     float* hr = h + (size_t)row * H;
     float ss = 0.f;
-    for (int k = threadIdx.x; k < H; k += blockDim.x) {
-        const float x = ok ? elem<T>::load(er, k) : 0.f;
-        hr[k] = x;
-        ss += x * x;
+    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
+        float4 x = load4<T>(er + k4);
+        if (!ok) x = make_float4(0.f, 0.f, 0.f, 0.f);
+        *(float4*)(hr + k4) = x;
+        ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
     }
     ss = block_sum(ss, red);
     const float inv = rsqrtf(ss / (float)H + eps);
-    for (int k = threadIdx.x; k < H; k += blockDim.x)
-        store_act<O>(out, (size_t)row * H + k, hr[k] * inv * elem<T>::load(gain, k));
+    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
+        const float4 x = *(const float4*)(hr + k4);
+        const float4 g = load4<T>(gain + k4);
+        store_act4<O>(out, (size_t)row * H + k4, make_float4(x.x * inv * g.x, x.y * inv * g.y, x.z * inv * g.z, x.w * inv * g.w));
+    }
 }
 
 // h[row] += sum_s P[s][row] (S > 1);  out[row] = RMSNorm(h[row]) * gain
@@ -83,11 +111,8 @@ __global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, 
     const float inv = rsqrtf(ss / (float)H + eps);
     for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
         const float4 x = *(const float4*)(hr + k4);
-        const size_t o = (size_t)row * H + k4;
-        store_act<O>(out, o, x.x * inv * elem<G>::load(gain, k4));
-        store_act<O>(out, o + 1, x.y * inv * elem<G>::load(gain, k4 + 1));
-        store_act<O>(out, o + 2, x.z * inv * elem<G>::load(gain, k4 + 2));
-        store_act<O>(out, o + 3, x.w * inv * elem<G>::load(gain, k4 + 3));
+        const float4 g = load4<G>(gain + k4);
+        store_act4<O>(out, (size_t)row * H + k4, make_float4(x.x * inv * g.x, x.y * inv * g.y, x.z * inv * g.z, x.w * inv * g.w));
     }
 }
 
@@ -629,9 +654,10 @@ static void embed_norm_t(const rows_t& r, const int32_t* tokA, int sA, const int
                          int V, float* h, const T* gain, float eps, void* out, act_t t, hipStream_t s)
 {
     const int R = r.B * r.n;
-    if (t == ACT_F32) k_embed_rmsnorm<T, float><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
-    else if (t == ACT_BF16) k_embed_rmsnorm<T, uint16_t><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
-    else k_embed_rmsnorm<T, _Float16><<<R, 256, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+    const int th = H >= 4096 ? 1024 : 256;
+    if (t == ACT_F32) k_embed_rmsnorm<T, float><<<R, th, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+    else if (t == ACT_BF16) k_embed_rmsnorm<T, uint16_t><<<R, th, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
+    else k_embed_rmsnorm<T, _Float16><<<R, th, 0, s>>>(r, tokA, sA, tokB, sB, E, H, V, h, gain, eps, out);
 }
 
 void launch_embed_rmsnorm(const rows_t& r, const int32_t* tokA, int sA, const int32_t* tokB, int sB, const void* E,
