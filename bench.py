@@ -56,7 +56,7 @@ def log(args, *a):
 SOURCES_OF_CLASS = {
     "attn_decode": ("common.h", "kernels.h", "kernels_model.hip"),
     "attn_verify": ("common.h", "kernels.h", "kernels_model.hip"),
-    "int4_proj": ("common.h", "kernels.h", "kernels_gemm.hip"),
+    "int4_proj": ("common.h", "kernels.h", "kernels_q4.hip"),
     "bf16_proj": ("common.h", "kernels.h", "kernels_gemm.hip"),
     "lm_head": ("common.h", "kernels.h", "kernels_gemm.hip"),
 }
@@ -90,9 +90,9 @@ def measured_traffic(kind: str):
 KERNEL_OF_CLASS = {
     "attn_decode": "k_attn_mfma<128, 1>",
     "attn_verify": "k_attn_mfma<128, 2>",
-    "int4_proj": "k_gemm_stream<0, 2, 4>",
-    "bf16_proj": "k_gemm_tiled<4>",
-    "lm_head": "k_gemm_stream<1, 2, 4> (draft rows), k_gemm_tiled<4> (verify rows)",
+    "int4_proj": "k_gemm_q4<2, 4>",
+    "bf16_proj": "k_gemm_tiled<5> (qkv, o, down), k_gemm_t32<4> (gate-up)",
+    "lm_head": "k_gemm_stream<2, 4> (draft rows), k_gemm_t32<4> (verify rows)",
 }
 
 

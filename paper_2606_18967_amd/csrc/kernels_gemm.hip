@@ -317,6 +317,117 @@ __global__ void __launch_bounds__(256) k_gemm_tiled(const uint16_t* __restrict__
         }
 }
 
+// The same tiling on v_mfma_f32_32x32x16_bf16 (MTW even): each wave's
+// (16 MTW) x 64 tile is MTW/2 x 2 blocks of 32 x 32; lane l reads row or
+// column l % 32 and k 8 (l / 32) + 0..7 of each 16-k step.
+template <int MTW>
+__global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+                                                    float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
+                                                    int ldc, int mode, int S, int mtiles, int total)
+{
+    constexpr int BM = 32 * MTW;
+    constexpr int AP = MTW;      // 16-byte A pieces per thread per stage (BM*8/256)
+    constexpr int WP = 4;        // 16-byte W pieces per thread per stage (128*8/256)
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * TLD];
+    __shared__ __attribute__((aligned(16))) uint16_t Ws[2][TBN * TLD];
+    const int per_xcd = gridDim.x >> 3;
+    const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (w >= total) return;
+    const int mt = w % mtiles, rest = w / mtiles;
+    const int s = rest % S, nt = rest / S;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1;
+    const int m0 = mt * BM, n0 = nt * TBN;
+    const int KS = K / TBK, Ks = KS / S, k0 = s * Ks, k1 = k0 + Ks;
+    const int rows = min(M - m0, BM);
+
+    u32x4 ra[2][AP], rw[2][WP];
+    auto load = [&](int kb, u32x4 (&a)[AP], u32x4 (&b)[WP]) {
+#pragma unroll
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            a[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)kb * TBK + col);
+        }
+#pragma unroll
+        for (int t = 0; t < WP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            b[t] = *(const u32x4*)(W + (size_t)(n0 + row) * K + (size_t)kb * TBK + col);
+        }
+    };
+    auto store = [&](int buf, const u32x4 (&a)[AP], const u32x4 (&b)[WP]) {
+#pragma unroll
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            *(u32x4*)(&As[buf][row * TLD + col]) = row < rows ? a[t] : (u32x4){0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int t = 0; t < WP; ++t) {
+            const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
+            *(u32x4*)(&Ws[buf][row * TLD + col]) = b[t];
+        }
+    };
+
+    floatx16 acc[MTW / 2][2];
+#pragma unroll
+    for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    load(k0, ra[0], rw[0]);
+    if (k0 + 1 < k1) load(k0 + 1, ra[1], rw[1]);
+    store(0, ra[0], rw[0]);
+    lds_barrier();
+    for (int kb = k0; kb < k1; kb += 2) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int k = kb + u;
+            if (k < k1) {
+                const int buf = (k - k0) & 1;
+                if (k + 2 < k1) load(k + 2, ra[u], rw[u]);      // slot u is free: stage k is in LDS
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const int kk = ks * 16 + (lane >> 5) * 8;
+                    u32x4 af[MTW / 2], bw[2];
+#pragma unroll
+                    for (int i = 0; i < MTW / 2; ++i)
+                        af[i] = *(const u32x4*)(&As[buf][(wm * 16 * MTW + 32 * i + (lane & 31)) * TLD + kk]);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        bw[j] = *(const u32x4*)(&Ws[buf][(wn * 64 + 32 * j + (lane & 31)) * TLD + kk]);
+#pragma unroll
+                    for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+                        for (int j = 0; j < 2; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[i]),
+                                                                               __builtin_bit_cast(bf16x8, bw[j]),
+                                                                               acc[i][j], 0, 0, 0);
+                }
+                if (k + 1 < k1) store(buf ^ 1, ra[u ^ 1], rw[u ^ 1]);
+                lds_barrier();
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = n0 + wn * 64 + 32 * j + (lane & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 16 * MTW + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row >= M) continue;
+                if (S == 1) {
+                    float* cp = C + (size_t)row * ldc + col;
+                    *cp = mode == GEMM_ADD ? *cp + acc[i][j][r] : acc[i][j][r];
+                } else {
+                    P[((size_t)s * M + row) * N + col] = acc[i][j][r];
+                }
+            }
+        }
+}
+
 // C[m][n] (+)= sum_s P[s][m][n]
 __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__ P, float* __restrict__ C, int M, int N,
                                                        int ldc, int S, int mode)
@@ -442,7 +553,7 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
         if (mtw == 5) k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
-        else k_gemm_tiled<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
+        else k_gemm_t32<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
