@@ -65,9 +65,9 @@ __device__ __forceinline__ float f16_bits_to_f32(uint16_t h) { return (float)__b
 // and shared by the four waves; each wave streams its weight columns from
 // HBM straight into registers through a ring of RD register sets (RD - 1
 // chunks in flight), so every weight byte is read once per m-tile.  Lane l
-// covers k = 128g + 32(l/16) + 8j + 0..7 of chunk g in k-step j
-// (v_mfma_f32_16x16x32_bf16), so its 64 bytes of a weight row are
-// contiguous; A is read from LDS in the same k order.  With several K splits
+// covers k = 128g + 32j + 8(l/16) + 0..7 of chunk g in k-step j
+// (v_mfma_f32_16x16x32_bf16): each load instruction reads 64 contiguous
+// bytes of 16 weight rows; A is read from LDS in the same k order.  With several K splits
 // the partial sums go to P[s][M][N] for the consumer (or k_splitk_reduce).
 // Work items are laid out so that consecutive ones (the m-tiles of one
 // column tile) land on the same XCD and share its L2.
@@ -75,12 +75,12 @@ constexpr int SK = 128;          // k per chunk
 constexpr int ALD = SK + 8;      // LDS row stride in 2-byte elements
 constexpr int SM = 64;           // rows per m-tile
 
-template <int NBW, int MT>
-__global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wt,
+template <int NBW, int MT, int NW>
+__global__ void __launch_bounds__(64 * NW) k_gemm_stream(const uint16_t* __restrict__ A, const uint16_t* __restrict__ Wt,
                                                      float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
                                                      int ldc, int mode, int S, int msup, int total)
 {
-    constexpr int RD = 3;
+    constexpr int RD = NW == 8 ? 4 : 3;   // register sets in the load ring (deeper where the registers allow)
     __shared__ __attribute__((aligned(16))) uint16_t As[2][SM * ALD];
     const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
@@ -90,27 +90,33 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int m0 = ms * SM;
     const int G = K / SK, Gs = G / S, g0 = s * Gs, g1 = g0 + Gs;
-    const int nb0 = (tile * 4 + wv) * NBW;
+    const int nb0 = (tile * NW + wv) * NBW;
     const int rows = min(M - m0, MT * 16);                  // rows staged (others stay zero)
+    // each work item walks its chunks from a different starting offset: in
+    // lockstep they would all read the same 256-byte column of the weight
+    // rows at once and crowd a few HBM channels
+    const int rot = (tile * 5 + s) % Gs;
+    auto phys = [&](int g) { const int i = g - g0 + rot; return g0 + (i >= Gs ? i - Gs : i); };
 
     // A tiles travel through a ring of register sets too (same depth as the
     // weights): the tile of chunk c + 1 is requested RD - 2 chunks before it
     // is stored to LDS
-    u32x4 ar[RD][4];
-    auto load_a = [&](int g, u32x4 (&a)[4]) {
+    constexpr int AP = 1024 / (64 * NW);                  // 16-byte A pieces per thread per chunk
+    u32x4 ar[RD][AP];
+    auto load_a = [&](int g, u32x4 (&a)[AP]) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int pidx = tid + t * 256;
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 64 * NW;
             const int row = pidx >> 4, col = (pidx & 15) * 8;
-            a[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)g * SK + col);
+            a[t] = *(const u32x4*)(A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)phys(g) * SK + col);
         }
     };
     // a tile of a chunk past the split (valid false) is stored as zeros, so
     // the padded iterations of the main loop add nothing
-    auto store_a = [&](int buf, const u32x4 (&a)[4], bool valid) {
+    auto store_a = [&](int buf, const u32x4 (&a)[AP], bool valid) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int pidx = tid + t * 256;
+        for (int t = 0; t < AP; ++t) {
+            const int pidx = tid + t * 64 * NW;
             const int row = pidx >> 4, col = (pidx & 15) * 8;
             if (row < MT * 16)
                 *(u32x4*)(&As[buf][row * ALD + col]) = (valid && row < rows) ? a[t] : (u32x4){0u, 0u, 0u, 0u};
@@ -120,9 +126,9 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     auto load_w = [&](int g, u32x4 (&wq)[NBW][4]) {
 #pragma unroll
         for (int i = 0; i < NBW; ++i) {
-            const uint16_t* wp = Wt + (size_t)((nb0 + i) * 16 + (lane & 15)) * K + (size_t)g * SK + 32 * (lane >> 4);
+            const uint16_t* wp = Wt + (size_t)((nb0 + i) * 16 + (lane & 15)) * K + (size_t)phys(g) * SK + 8 * (lane >> 4);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) wq[i][j] = *(const u32x4*)(wp + 8 * j);
+            for (int j = 0; j < 4; ++j) wq[i][j] = *(const u32x4*)(wp + 32 * j);
         }
     };
 
@@ -135,7 +141,7 @@ __global__ void __launch_bounds__(256) k_gemm_stream(const uint16_t* __restrict_
     auto compute = [&](int buf, const u32x4 (&wq)[NBW][4]) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint16_t* ab = &As[buf][(lane & 15) * ALD + 32 * (lane >> 4) + 8 * j];
+            const uint16_t* ab = &As[buf][(lane & 15) * ALD + 32 * j + 8 * (lane >> 4)];
             u32x4 af[MT];
 #pragma unroll
             for (int t = 0; t < MT; ++t) af[t] = *(const u32x4*)(ab + t * 16 * ALD);
@@ -530,15 +536,16 @@ size_t gemm_part_floats(int M, int N, int K)
     return S > 1 ? (size_t)S * M * N : 0;
 }
 
-template <int NBW>
+template <int NBW, int NW>
 static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const uint16_t* W, float* C, float* P, int M,
                       int N, int K, int ldc, int mode, int S, int msup, int total)
 {
+    constexpr int T = 64 * NW;
     switch (MT) {
-        case 1: k_gemm_stream<NBW, 1><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        case 2: k_gemm_stream<NBW, 2><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        case 3: k_gemm_stream<NBW, 3><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
-        default: k_gemm_stream<NBW, 4><<<grid, 256, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 1: k_gemm_stream<NBW, 1, NW><<<grid, T, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 2: k_gemm_stream<NBW, 2, NW><<<grid, T, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        case 3: k_gemm_stream<NBW, 3, NW><<<grid, T, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
+        default: k_gemm_stream<NBW, 4, NW><<<grid, T, 0, s>>>(A, W, C, P, M, N, K, ldc, mode, S, msup, total); break;
     }
 }
 
@@ -565,11 +572,16 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
     if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
     int msup = (M + SM - 1) / SM;
     int MT = msup > 1 ? 4 : (M + 15) / 16;
-    int tiles = N / (64 * nbw);
+    // 8-wave work-groups (twice the columns, one A tile for twice the waves)
+    // when 4-wave ones would not all be resident at once (two per CU): the
+    // draft LM head then runs in a single wave of work-groups
+    const bool wide = nbw == 2 && N % 256 == 0 && (N / 128) * S * msup > 512;
+    int tiles = N / (64 * nbw * (wide ? 2 : 1));
     int total = tiles * S * msup;
     dim3 grid((total + 7) / 8 * 8);
-    if (nbw == 2) stream_mt<2>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
-    else stream_mt<1>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
+    if (wide) stream_mt<2, 8>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
+    else if (nbw == 2) stream_mt<2, 4>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
+    else stream_mt<1, 4>(MT, grid, s, A, W, C, part, M, N, K, ldc, mode, S, msup, total);
     if (S > 1 && !defer_reduce) {
         size_t MN = (size_t)M * N;
         k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
