@@ -201,6 +201,14 @@ sd_status sd_timing(sd_engine e, int32_t on);
  * kernel time in milliseconds and the number of launches (host pointers). */
 sd_status sd_timing_read(sd_engine e, int32_t cls, double* total_ms, int32_t* launches);
 
+/* Dense GEMM with the library's bf16 kernels, for the F_eff microbenchmark
+ * of the cost-model calibration (App. D.2: effective compute throughput from
+ * repeated dense matrix multiplications).  C[M][N] (fp32, row stride N) =
+ * A[M][K] (bf16, row-major) x W[N][K]^T (bf16, row-major); device pointers,
+ * caller-owned.  Needs N % 128 == 0 and K % 128 == 0; M >= 1.  No split-K
+ * (no workspace).  Enqueued on `stream`. */
+sd_status sd_dense_gemm_bf16(const void* A, const void* W, float* C, int32_t M, int32_t N, int32_t K, void* stream);
+
 /* ------------------------------------------------ host policy (no GPU) */
 
 /* Roofline cost model of Sec. 4.2 / App. D.2.  Architecture terms: W_T, W_D

@@ -543,6 +543,18 @@ extern "C" sd_status sd_sync(sd_engine e, void* stream)
     return SD_OK;
 }
 
+extern "C" sd_status sd_dense_gemm_bf16(const void* A, const void* W, float* C, int32_t M, int32_t N, int32_t K,
+                                        void* stream)
+{
+    if (!A || !W || !C) return fail(SD_E_INVAL, "NULL argument");
+    if (M < 1 || N < 128 || K < 128 || N % 128 || K % 128)
+        return fail(SD_E_UNSUPPORTED, "need M >= 1 and N, K positive multiples of 128");
+    launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)W, C, nullptr, 0, M, N, K, N, GEMM_STORE, false,
+                     (hipStream_t)stream);
+    HIP_TRY(hipGetLastError());
+    return SD_OK;
+}
+
 extern "C" sd_status sd_timing(sd_engine e, int32_t on)
 {
     if (!e) return fail(SD_E_INVAL, "engine is NULL");

@@ -30,7 +30,7 @@ API_SYMBOLS = (
     "sd_bind_kv", "sd_drafter_bytes", "sd_refresh_drafter", "sd_prefill", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
-    "sd_alpha_from_tau", "sd_timing", "sd_timing_read",
+    "sd_alpha_from_tau", "sd_timing", "sd_timing_read", "sd_dense_gemm_bf16",
 )
 
 # kernel classes of sd_timing_read
@@ -97,6 +97,7 @@ def lib():
             "sd_set_debug": (_i32, [_P, _i32]),
             "sd_timing": (_i32, [_P, _i32]),
             "sd_timing_read": (_i32, [_P, _i32, _P, _P]),
+            "sd_dense_gemm_bf16": (_i32, [_P, _P, _P, _i32, _i32, _i32, _P]),
             "sd_cost_init": (_i32, [_P, _d, _d, _d, _P]),
             "sd_cost_times": (_i32, [_P, _d, _d, _i32, _P, _P, _P]),
             "sd_toggle": (_i32, [_P, _i32, _d, _d, _i32, _d, _P]),
@@ -313,6 +314,14 @@ def sd_step(eng: Engine, bufs: SDBuffers, slots, last_tok, T, seed, step):
     eng.accept(slots, bufs.draft_tok, bufs.q_logits, bufs.q_stats, bufs.p_logits, g, T, seed, step,
                bufs.out_tok, bufs.n_emit, bufs.next_tok)
     eng.rollback(slots, bufs.n_emit)
+
+
+def dense_gemm_bf16(A: torch.Tensor, W: torch.Tensor, out: torch.Tensor):
+    """out[M][N] (fp32) = A[M][K] W[N][K]^T with the library's bf16 GEMM kernels."""
+    M, K = A.shape
+    N = W.shape[0]
+    _check(lib().sd_dense_gemm_bf16(_dev(A, "A", torch.bfloat16, (M, K)), _dev(W, "W", torch.bfloat16, (N, K)),
+                                    _dev(out, "out", torch.float32, (M, N)), M, N, K, _stream()))
 
 
 # -------------------------------------------------------------------- host policy
