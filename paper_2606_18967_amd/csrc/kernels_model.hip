@@ -303,7 +303,7 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 }
 
 // MFMA attention for a bf16 cache.  Work-group (b, kv head, chunk, query-row
-// slice z): a sequence's context is split evenly into ceil(ctx / MCH) chunks
+// slice z): a sequence's context is split evenly into ceil(ctx / ch) chunks
 // and each wave takes a quarter of its chunk in blocks of 32 positions.  Per
 // block:
 //   S^T = K Q^T with v_mfma_f32_16x16x32_bf16: K rows straight from global
@@ -320,16 +320,22 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 // than 8, bounding the exp2 terms by 256); the four waves are merged
 // through LDS and the chunk result (m in natural-log units, l, o[d]) goes to
 // the same partial buffer k_attn_combine reads.
-#ifndef ATT_MFMA_CHUNK
-#define ATT_MFMA_CHUNK 1024
+// Chunk length of the MFMA kernel, chosen per launch: enough chunks per
+// sequence for about ATT_TARGET_WGS work-groups in all (two per CU), each at
+// least ATT_MIN_CHUNK positions, so a large batch streams a whole context per
+// work-group and a small one still fills the GPU.
+#ifndef ATT_TARGET_WGS
+#define ATT_TARGET_WGS 512
 #endif
-constexpr int MCH = ATT_MFMA_CHUNK;   // positions per work-group
+#ifndef ATT_MIN_CHUNK
+#define ATT_MIN_CHUNK 512
+#endif
 
 // two waves per SIMD where the registers allow it without spills (one query
 // tile); the verify variants keep one
 template <int D, int MQ>
 __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
-                                                   const uint16_t* vc, int layer, float* part, int max_chunks)
+                                                   const uint16_t* vc, int layer, float* part, int max_chunks, int ch)
 {
     constexpr int KS = D / 32;      // k-steps over the head dim
     constexpr int NBD = D / 16;     // 16-wide blocks of the head dim
@@ -347,9 +353,9 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     const int basepos = __builtin_amdgcn_readfirstlane(r.kv_len[slot]) + r.off;
     int ctx = basepos + r.n;
     if (ctx > r.max_ctx) ctx = r.max_ctx;
-    // the sequence's ceil(ctx / MCH) chunks (the count k_attn_combine reads)
+    // the sequence's ceil(ctx / ch) chunks (the count k_attn_combine reads)
     // split its context evenly, in multiples of 32 positions
-    const int nch = (ctx + MCH - 1) / MCH;
+    const int nch = (ctx + ch - 1) / ch;
     const int clen = ((ctx + nch - 1) / nch + 31) & ~31;
     const int p0 = c * clen;
     if (p0 >= ctx) return;
@@ -359,32 +365,11 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     const int G = n_q / n_kv, QR = G * r.n;
     const int qbase = z * 16 * MQ;
 
-    // Q^T fragments (B operand of S^T = K Q^T); rows past QR read row 0 and are zeroed
+    // Q^T fragments (B operand of S^T = K Q^T), filled after the first K/V
+    // loads are issued so that the two memory round trips overlap
     const float qscale = 1.4426950408889634f * rsqrtf((float)D);
     bf16x8 qf[MQ][KS];
     int lim[MQ];
-#pragma unroll
-    for (int mt = 0; mt < MQ; ++mt) {
-        const int qrow = qbase + 16 * mt + lr;
-        const bool live = qrow < QR;
-        const int qr = live ? qrow : 0;
-        const int g = qr / r.n, i = qr - g * r.n;
-        lim[mt] = live ? basepos + i : -1;
-        const float sc = live ? qscale : 0.f;
-        const float4* qp = (const float4*)(q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D);
-        float4 qv[KS][2];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            qv[ks][0] = qp[2 * (4 * ks + cq)];
-            qv[ks][1] = qp[2 * (4 * ks + cq) + 1];
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const float4 a = qv[ks][0], c2 = qv[ks][1];
-            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){pack_bf16x2(a.x * sc, a.y * sc), pack_bf16x2(a.z * sc, a.w * sc),
-                                                            pack_bf16x2(c2.x * sc, c2.y * sc), pack_bf16x2(c2.z * sc, c2.w * sc)});
-        }
-    }
 
     const size_t cbase = ((((size_t)layer * r.max_slots + slot) * n_kv + kvh) * (size_t)r.max_ctx) * D;
     const uint16_t* K = kc + cbase;
@@ -511,6 +496,30 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     // two register sets: the next block's K and V load while this one computes
     u32x4 kf0[2][KS], kf1[2][KS], vv0[CPP / 2], vv1[CPP / 2];
     load_kv(wq0, kf0, vv0);
+    // rows past QR read row 0 and are zeroed
+#pragma unroll
+    for (int mt = 0; mt < MQ; ++mt) {
+        const int qrow = qbase + 16 * mt + lr;
+        const bool live = qrow < QR;
+        const int qr = live ? qrow : 0;
+        const int g = qr / r.n, i = qr - g * r.n;
+        lim[mt] = live ? basepos + i : -1;
+        const float sc = live ? qscale : 0.f;
+        const float4* qp = (const float4*)(q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D);
+        float4 qv[KS][2];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            qv[ks][0] = qp[2 * (4 * ks + cq)];
+            qv[ks][1] = qp[2 * (4 * ks + cq) + 1];
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const float4 a = qv[ks][0], c2 = qv[ks][1];
+            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){pack_bf16x2(a.x * sc, a.y * sc), pack_bf16x2(a.z * sc, a.w * sc),
+                                                            pack_bf16x2(c2.x * sc, c2.y * sc), pack_bf16x2(c2.z * sc, c2.w * sc)});
+        }
+    }
+
     for (int blk = wq0; blk < wq1; blk += 64) {
         load_kv(blk + 32, kf1, vv1);
         block(blk, kf0, vv0);
@@ -699,7 +708,7 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, co
                                                  (uint16_t*)c.v, layer, q_out, upw);
 }
 
-int attention_chunk() { return ATT_CH < MCH ? ATT_CH : MCH; }
+int attention_chunk() { return ATT_CH < ATT_MIN_CHUNK ? ATT_CH : ATT_MIN_CHUNK; }
 
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
 {
@@ -711,21 +720,30 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
                          int max_chunks, hipStream_t s)
 {
     if constexpr (sizeof(T) == 2) {
-        // bf16 cache: MFMA kernel, chunks of MCH positions (max_chunks counts ATT_CH chunks, ATT_CH <= MCH)
+        // bf16 cache: MFMA kernel.  max_chunks (the partial buffer's chunk
+        // capacity) counts chunks of attention_chunk() <= ATT_MIN_CHUNK positions.
         const int QR = (n_q / c.n_kv) * r.n;
         const int MQ = QR > 48 ? 4 : (QR + 15) / 16;
         const int zs = (QR + 16 * MQ - 1) / (16 * MQ);
-        const int mch = (max_chunks * ATT_CH + MCH - 1) / MCH;
+        const int per_chunk = r.B * c.n_kv * zs;                       // work-groups per chunk index
+        const int want = (ATT_TARGET_WGS + per_chunk - 1) / per_chunk;   // chunks per sequence at capacity
+        int ch = (r.max_ctx + want - 1) / want;
+        ch = ((ch > ATT_MIN_CHUNK ? ch : ATT_MIN_CHUNK) + 31) & ~31;
+        int mch = (r.max_ctx + ch - 1) / ch;
+        if (mch > max_chunks) {                                          // cannot happen for ch >= attention_chunk()
+            mch = max_chunks;
+            ch = ((r.max_ctx + mch - 1) / mch + 31) & ~31;
+        }
         dim3 grid(r.B * c.n_kv, mch, zs);
         const uint16_t* kc = (const uint16_t*)c.k;
         const uint16_t* vc = (const uint16_t*)c.v;
         switch (MQ) {
-            case 1: k_attn_mfma<D, 1><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
-            case 2: k_attn_mfma<D, 2><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
-            case 3: k_attn_mfma<D, 3><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
-            default: k_attn_mfma<D, 4><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch); break;
+            case 1: k_attn_mfma<D, 1><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
+            case 2: k_attn_mfma<D, 2><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
+            case 3: k_attn_mfma<D, 3><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
+            default: k_attn_mfma<D, 4><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
         }
-        return attn_split{mch, MCH};
+        return attn_split{mch, ch};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
         k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
