@@ -78,8 +78,10 @@ def _declare(L):
         "or_accept_seq": (_i, [_i, _i, _f, _P, _P, _P, _u64, _u64, _u32, _u32, _P, _P, _P, _P]),
         "or_quantize_rtn4": (None, [_P, _i, _i, _i, _P, _P]),
         "or_quantize_rtn4_asym": (None, [_P, _i, _i, _i, _P, _P, _P]),
+        "or_quantize_rtn8": (None, [_P, _i, _i, _i, _P, _P]),
         "or_model_new": (_P, [_P, _i, _P]),
         "or_model_set_q4": (None, [_P, _i, _i, _P, _P, _i]),
+        "or_model_set_quant": (None, [_P, _i, _i, _P, _P, _P, _i]),
         "or_model_free": (None, [_P]),
         "or_forward_seq": (None, [_P, _P, _P, _i, _P, _i, _i, _P]),
         "or_sd_step_seq": (_i, [_P, _P, _P, _P, _i, _i, _i32, _i, _f, _u64, _u64, _u32,
@@ -183,6 +185,30 @@ def quantize_rtn4_asym(w: np.ndarray, group: int = 128):
     return codes, scales, zeros
 
 
+def quantize_rtn8(w: np.ndarray, group: int = 128):
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    N, K = w.shape
+    codes = np.zeros((N, K), dtype=np.int8)
+    scales = np.zeros((N, K // group), dtype=np.uint16)
+    lib().or_quantize_rtn8(_ptr(w), N, K, group, _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+# drafter formats: RTN int4 symmetric (the default), int4 asymmetric, int8 symmetric
+DRAFTER_FORMATS = ("w4", "w4a", "w8")
+
+
+def quantize(w: np.ndarray, fmt: str = "w4", group: int = 128):
+    """(codes, scales, zeros or None) of one weight matrix in drafter format fmt."""
+    if fmt == "w4":
+        return (*quantize_rtn4(w, group), None)
+    if fmt == "w4a":
+        return quantize_rtn4_asym(w, group)
+    if fmt == "w8":
+        return (*quantize_rtn8(w, group), None)
+    raise ValueError(f"unknown drafter format {fmt!r}")
+
+
 def f16_bits_to_f32(h: np.ndarray) -> np.ndarray:
     return np.ascontiguousarray(h, dtype=np.uint16).view(np.float16).astype(np.float32)
 
@@ -212,6 +238,13 @@ class Model:
         self._keep += [codes, scales]
         lib().or_model_set_q4(self.h, layer, which, _ptr(codes), _ptr(scales), group)
 
+    def set_quant(self, layer: int, which: int, codes: np.ndarray, scales: np.ndarray, zeros=None, group=128):
+        codes = np.ascontiguousarray(codes).astype(np.int8)       # asymmetric codes 0..15 fit in int8
+        scales = np.ascontiguousarray(scales, dtype=np.uint16)
+        zeros = None if zeros is None else np.ascontiguousarray(zeros, dtype=np.uint8)
+        self._keep += [codes, scales] + ([zeros] if zeros is not None else [])
+        lib().or_model_set_quant(self.h, layer, which, _ptr(codes), _ptr(scales), _ptr(zeros), group)
+
     def __del__(self):
         try:
             if getattr(self, "h", None):
@@ -235,13 +268,17 @@ def tensor_f32(t: np.ndarray, wkind: int) -> np.ndarray:
     return np.ascontiguousarray(t, dtype=np.float32)
 
 
-def make_drafter(cfg: dict, tensors, wkind: int, group: int = 128) -> Model:
-    """RTN-W4 drafter: the same network with QKVO/FFN projections replaced
-    by their int4 group-`group` codes (Sec. 4.1)."""
+def make_drafter(cfg: dict, tensors, wkind: int, group: int = 128, fmt: str = "w4") -> Model:
+    """RTN drafter: the same network with QKVO/FFN projections replaced by
+    their group-`group` RTN codes (Sec. 4.1), int4 symmetric by default,
+    int4 asymmetric ("w4a") or int8 ("w8") on request."""
     d = Model(cfg, tensors, wkind)
     for l, which, ti in d.quant_targets():
-        codes, scales = quantize_rtn4(tensor_f32(tensors[ti], wkind), group)
-        d.set_q4(l, which, codes, scales, group)
+        codes, scales, zeros = quantize(tensor_f32(tensors[ti], wkind), fmt, group)
+        if zeros is None and fmt == "w4":
+            d.set_q4(l, which, codes, scales, group)
+        else:
+            d.set_quant(l, which, codes, scales, zeros, group)
     return d
 
 

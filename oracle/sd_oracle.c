@@ -274,6 +274,9 @@ OR_API int or_accept_seq(int V, int gamma, float T,
 /* Also the asymmetric variant the paper mentions:                          */
 /*   s = fp16((max - min) / 15), z = clamp(rint(-min / s), 0, 15),           */
 /*   q = clamp(rint(w / s) + z, 0, 15), w^ = s * (q - z).                    */
+/* And the 8-bit drafter of the W4-versus-W8 comparison (App. B.3, Table 4), */
+/* symmetric like the 4-bit default:                                         */
+/*   s = fp16(max|w_g| / 127), q = clamp(rint(w / s), -128, 127).            */
 /* ------------------------------------------------------------------------ */
 
 OR_API void or_quantize_rtn4(const float* w, int N, int K, int group,
@@ -327,6 +330,30 @@ OR_API void or_quantize_rtn4_asym(const float* w, int N, int K, int group,
         }
 }
 
+OR_API void or_quantize_rtn8(const float* w, int N, int K, int group,
+                             int8_t* codes /* [N][K] */, uint16_t* scales /* [N][K/group] */)
+{
+    int G = K / group;
+    for (int n = 0; n < N; ++n)
+        for (int g = 0; g < G; ++g) {
+            const float* wg = w + (size_t)n * K + (size_t)g * group;
+            float amax = 0.0f;
+            for (int i = 0; i < group; ++i) { float a = fabsf(wg[i]); if (a > amax) amax = a; }
+            uint16_t sh = or_f32_to_f16(amax / 127.0f);
+            float s = or_f16_to_f32(sh);
+            scales[(size_t)n * G + g] = sh;
+            int8_t* cg = codes + (size_t)n * K + (size_t)g * group;
+            for (int i = 0; i < group; ++i) {
+                int q = 0;
+                if (s != 0.0f) {
+                    float r = rintf(wg[i] / s);
+                    q = r < -128.0f ? -128 : (r > 127.0f ? 127 : (int)r);
+                }
+                cg[i] = (int8_t)q;
+            }
+        }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Decoder forward (Llama-style, the architecture the workloads use):        */
 /*   a = RMSNorm(h) * g1;  q,k,v = a Wq^T, a Wk^T, a Wv^T;                  */
@@ -354,6 +381,7 @@ typedef struct {
     const void* w;          /* OR_F32: float[N][K]; OR_BF16: uint16[N][K] */
     const int8_t* codes;    /* OR_Q4: int8[N][K] */
     const uint16_t* scales; /* OR_Q4: fp16[N][K/group] */
+    const uint8_t* zeros;   /* OR_Q4: zero points [N][K/group], or NULL (symmetric) */
 } or_lin;
 
 typedef struct {
@@ -375,7 +403,8 @@ static double vec_at(int kind, const void* p, size_t i)
     return kind == OR_BF16 ? bf16_to_f64(((const uint16_t*)p)[i]) : (double)((const float*)p)[i];
 }
 
-/* Row n of W as doubles (the q4 kind dequantizes s * q group by group). */
+/* Row n of W as doubles (the quantized kind dequantizes s * (q - z) group by
+   group, z = 0 for the symmetric formats). */
 static void lin_row(const or_lin* L, size_t n, double* wrow)
 {
     size_t K = (size_t)L->K;
@@ -383,7 +412,8 @@ static void lin_row(const or_lin* L, size_t n, double* wrow)
         size_t G = K / (size_t)L->group;
         for (size_t g = 0; g < G; ++g) {
             double s = (double)or_f16_to_f32(L->scales[n * G + g]);
-            for (size_t k = g * L->group; k < (g + 1) * L->group; ++k) wrow[k] = s * (double)L->codes[n * K + k];
+            double z = L->zeros ? (double)L->zeros[n * G + g] : 0.0;
+            for (size_t k = g * L->group; k < (g + 1) * L->group; ++k) wrow[k] = s * ((double)L->codes[n * K + k] - z);
         }
     } else if (L->kind == OR_BF16) {
         for (size_t k = 0; k < K; ++k) wrow[k] = bf16_to_f64(((const uint16_t*)L->w)[n * K + k]);
@@ -476,7 +506,16 @@ OR_API void or_model_set_q4(or_model* m, int l, int which, const int8_t* codes,
                             const uint16_t* scales, int group)
 {
     or_lin* L = which == 0 ? &m->qkv[l] : which == 1 ? &m->o[l] : which == 2 ? &m->gu[l] : &m->dn[l];
-    L->kind = OR_Q4; L->codes = codes; L->scales = scales; L->group = group;
+    L->kind = OR_Q4; L->codes = codes; L->scales = scales; L->zeros = NULL; L->group = group;
+}
+
+/* The same for any RTN format: integer codes (int4, asymmetric int4 or int8),
+   fp16 scales and, for the asymmetric format, zero points (else NULL). */
+OR_API void or_model_set_quant(or_model* m, int l, int which, const int8_t* codes,
+                               const uint16_t* scales, const uint8_t* zeros, int group)
+{
+    or_lin* L = which == 0 ? &m->qkv[l] : which == 1 ? &m->o[l] : which == 2 ? &m->gu[l] : &m->dn[l];
+    L->kind = OR_Q4; L->codes = codes; L->scales = scales; L->zeros = zeros; L->group = group;
 }
 
 OR_API void or_model_free(or_model* m)
