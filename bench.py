@@ -3,7 +3,8 @@
 
 Workload: the 8B-shaped decoder (4 layers, hidden 4096, 32 query / 8 KV heads
 x 128, SwiGLU FFN 14336, vocab 128256, bf16, random init), int4 group-128
-drafter refreshed from it, B = 64 sequences with 2048 positions of random
+drafter refreshed from it (or, with --drafter, its asymmetric-int4 or int8
+variant), B = 64 sequences with 2048 positions of random
 bf16 KV context each, gamma = 4, temperature 1.0.  One step = gamma draft
 forwards + one verify forward over B*(gamma+1) positions + accept + KV
 rollback + the host read of n_emit.  The metric is accepted (emitted)
@@ -38,6 +39,8 @@ def parse():
     ap.add_argument("--ar-steps", type=int, default=20)
     ap.add_argument("--cpu-seqs", type=int, default=12, help="sequences in the oracle's CPU sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--drafter", choices=("w4", "w4a", "w8"), default="w4",
+                    help="drafter format: RTN int4 symmetric (default), int4 asymmetric, int8")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -90,13 +93,17 @@ def measured_traffic(kind: str):
 KERNEL_OF_CLASS = {
     "attn_decode": "k_attn_mfma<128, 1>",
     "attn_verify": "k_attn_mfma<128, 2>",
-    "int4_proj": "k_gemm_q4<2, 4>",
+    "int4_proj": "k_gemm_q4<2, 4, 0>",
     "bf16_proj": "k_gemm_tiled<5> (qkv, o, down), k_gemm_t32<4> (gate-up)",
     "lm_head": "k_gemm_stream<2, 4> (draft rows), k_gemm_t32<4> (verify rows)",
 }
 
 
-def algorithmic_per_launch(cfg, B, gamma, ctx):
+# bytes per quantized weight: codes + fp16 scale (+ zero point) per group of 128
+DRAFTER_BYTES_PER_WEIGHT = {"w4": 0.5 + 2 / 128, "w4a": 0.5 + 3 / 128, "w8": 1 + 2 / 128}
+
+
+def algorithmic_per_launch(cfg, B, gamma, ctx, drafter="w4"):
     """Bytes (HBM-bound classes) or FLOPs (MFMA-bound) one launch of each
     timing class must move or do, for a mean cached length ctx (kv_len at the
     start of the step): the sizes of what the operation reads and writes, not
@@ -108,7 +115,7 @@ def algorithmic_per_launch(cfg, B, gamma, ctx):
     attn_d = B * kv_pos * (ctx + (gamma + 1) / 2) + B * q_row
     attn_v = B * kv_pos * (ctx + gamma + 1) + B * (gamma + 1) * q_row
     w_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F          # projection weights per layer
-    q4 = (w_layer * 0.5 + w_layer / 128 * 2) / 4                         # mean int4 launch (4 per layer)
+    q4 = w_layer * DRAFTER_BYTES_PER_WEIGHT[drafter] / 4                # mean drafter launch (4 per layer)
     rows_v = B * (gamma + 1)
     proj_flops = 2 * rows_v * w_layer / 4                                 # mean verify projection launch
     lm = V * H * 2 + (gamma * B + rows_v) / (gamma + 1) * (H * 2 + V * 4)
@@ -225,10 +232,15 @@ def main():
     synth.fill_kv_context(k, v, S, seed + 100)
     kv_len.fill_(S)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    qbuf = eng.refresh_drafter()
+    # drafter refresh (the per-training-step Prep): once to load the kernels,
+    # then timed with events on the stream it runs on
+    qbuf = eng.refresh_drafter(fmt=args.drafter)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    eng.refresh_drafter(qbuf, fmt=args.drafter)
+    ev1.record()
     torch.cuda.synchronize()
-    prep_ms = (time.perf_counter() - t0) * 1e3
+    prep_ms = ev0.elapsed_time(ev1)
 
     slots = torch.arange(B, dtype=torch.int32, device=dev)
     bufs = sdrl.SDBuffers(eng, B, gamma)
@@ -309,7 +321,7 @@ def main():
     H, V, d, nkv, nq, F, L = (cfg[x] for x in ("hidden", "vocab", "head_dim", "n_kv", "n_q", "ffn", "n_layers"))
     ctx_prof = 0.5 * (kv_before + kv_after)             # mean kv_len at the start of the profiled steps
     dom = max(classes, key=lambda c: classes[c]["ms_per_step"])
-    algo = algorithmic_per_launch(cfg, B, gamma, ctx_prof)
+    algo = algorithmic_per_launch(cfg, B, gamma, ctx_prof, args.drafter)
     bound, amount = algo.get(dom, ("hbm", float("nan")))
     us = classes[dom]["us_per_launch"]
     if bound == "hbm":
@@ -329,7 +341,7 @@ def main():
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed)
+        cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, args.drafter)
 
     rec = {
         "metric": "accepted tokens/s per GPU per SD step",
@@ -344,8 +356,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + int4 g128 drafter, B=64, "
-                               "KV context 2048 (random N(0,1)), gamma=4, T=1.0",
+        "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + "
+                               + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
+                               + " drafter, B=64, KV context 2048 (random N(0,1)), gamma=4, T=1.0",
+                   "drafter": args.drafter,
                    "batch": B, "context": S, "gamma": gamma, "temperature": T, "layers": L, "hidden": H,
                    "heads": f"{nq}q/{nkv}kv x {d}", "ffn": F, "vocab": V},
         "roofline": roof,
@@ -363,7 +377,7 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed):
+def cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, fmt="w4"):
     """The oracle (plain C, OpenMP over projection rows) on the host: one SD
     step for the first `cpu_seqs` sequences of the workload, from the same
     weights and KV context."""
@@ -375,7 +389,7 @@ def cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed):
     log(args, "cpu baseline: copying weights to host ...")
     Wh = [synth.to_numpy_bits(w) for w in W]
     target = oracle.Model(cfg, Wh, oracle.BF16)
-    drafter = oracle.make_drafter(cfg, Wh, oracle.BF16)
+    drafter = oracle.make_drafter(cfg, Wh, oracle.BF16, fmt=fmt)
     cap = S + gamma + 2
     toks = synth.make_tokens(64, 1, cfg["vocab"], seed + 7)[:, 0].numpy()   # the workload's first tokens
     emitted, elapsed = 0, 0.0

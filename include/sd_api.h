@@ -110,24 +110,49 @@ size_t sd_kv_bytes(const sd_model_cfg* cfg, int32_t max_slots, int32_t max_ctx);
  * (device int32[max_slots]).  K holds post-RoPE keys. */
 sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len);
 
-/* Bytes of the quantized drafter for cfg: for each layer, the projections
- * qkv, o, gu, down in that order, each as packed int4 codes (N*K/2 bytes)
- * followed by fp16 scales (N*K/64 bytes), every block 256-byte aligned.
- * Packed layout: see sd_refresh_drafter. */
+/* Drafter weight formats (RTN, groups of 128 weights along K, one fp16 scale
+ * per (output column, group)): int4 symmetric (Sec. 4.1, the default), int4
+ * asymmetric with a zero point per (column, group) (App. B.2), and int8
+ * symmetric (the W8 drafter of App. B.3 / Table 4). */
+typedef enum { SD_DRAFT_W4 = 0, SD_DRAFT_W4A = 1, SD_DRAFT_W8 = 2 } sd_draft_fmt;
+
+/* Bytes of the quantized drafter for cfg in format fmt (0 for an unknown
+ * format): for each layer, the projections qkv, o, gu, down in that order,
+ * each as packed codes (N*K/2 bytes for int4, N*K for int8), then fp16
+ * scales (N*K/64 bytes), then for SD_DRAFT_W4A one zero-point byte per
+ * (column, group) (N*K/128 bytes), every block 256-byte aligned.  Packed
+ * layout: see sd_refresh_drafter_fmt. */
+size_t sd_drafter_bytes_fmt(const sd_model_cfg* cfg, int32_t fmt);
+
+/* sd_drafter_bytes_fmt(cfg, SD_DRAFT_W4). */
 size_t sd_drafter_bytes(const sd_model_cfg* cfg);
 
 /* Drafter refresh (Sec. 4.1; Algorithm 1 does it at the start of every
- * training step): RTN int4 quantization of Wqkv, Wo, Wgu, Wdown of every
- * layer of the bound target into qbuf (device, >= sd_drafter_bytes).
- * Embedding, norms and LM head are shared with the target, unquantized.
- * Per group of 128 weights of one row: s = fp16(max|w|/7),
- * q = clamp(rint(w/s), -8, 7).  Packed layout per matrix [N][K] (N a
- * multiple of 32, G = K/128): for column block nb = n/32 and group
- * g = k/128, 512 uint32 words; lane l = n%32 + 32*h (h = 0, 1) holds for
- * k-step st = 0..7 the word with the 8 codes k = 128g + 16st + 8h + e,
- * code e in the nibble at bit 4*(e/2) + 16*(e%2), stored as q + 8, at word
- * index (((nb*G + g)*2 + st/4)*64 + l)*4 + st%4; scale index
- * (nb*G + g)*32 + n%32.  Must be called again after the weights change. */
+ * training step): RTN quantization of Wqkv, Wo, Wgu, Wdown of every layer of
+ * the bound target, in format fmt, into qbuf (device, 16-byte aligned,
+ * >= sd_drafter_bytes_fmt(cfg, fmt) bytes, owned by the caller and read by
+ * every later sd_draft).  Embedding, norms and LM head are shared with the
+ * target, unquantized.  Per group of 128 weights of one row:
+ *   SD_DRAFT_W4:  s = fp16(max|w|/7), q = clamp(rint(w/s), -8, 7);
+ *   SD_DRAFT_W4A: s = fp16((max-min)/15), z = clamp(rint(-min/s), 0, 15),
+ *                 q = clamp(rint(w/s) + z, 0, 15), weight s*(q - z);
+ *   SD_DRAFT_W8:  s = fp16(max|w|/127), q = clamp(rint(w/s), -128, 127)
+ * (q = z = 0 when s = 0; fp32 arithmetic, round half to even).
+ * Packed layout per matrix [N][K] (N a multiple of 32, G = K/128), for
+ * column block nb = n/32 and group g = k/128; lane l = n%32 + 32*h (h = 0, 1)
+ * stands for the codes k = 128g + 16st + 8h + e, st = 0..7, e = 0..7:
+ *   int4: code e of k-step st in the nibble at bit 4*(e/2) + 16*(e%2) of
+ *         word (((nb*G + g)*2 + st/4)*64 + l)*4 + st%4, stored as q + 8
+ *         (W4) or q (W4A);
+ *   int8: code e of k-step st in byte e%4 of word j = 2*st + e/4 at index
+ *         (((nb*G + g)*4 + j/4)*64 + l)*4 + j%4, stored as q + 128.
+ * Scale and zero point of (n, g) at index (nb*G + g)*32 + n%32.  Errors:
+ * SD_E_INVAL (NULL, misaligned or short qbuf, unknown fmt), SD_E_STATE
+ * (weights not bound).  Must be called again after the weights change; a
+ * failed refresh leaves the engine without a drafter. */
+sd_status sd_refresh_drafter_fmt(sd_engine e, int32_t fmt, void* qbuf, size_t bytes, void* stream);
+
+/* sd_refresh_drafter_fmt(e, SD_DRAFT_W4, qbuf, bytes, stream). */
 sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream);
 
 /* --------------------------------------------------------- the SD step */

@@ -80,39 +80,75 @@ def compare_ar(x_oracle: int, gap: float, p_oracle, x_dev: int, p_dev, tol: floa
     raise Mismatch(f"AR token: dev {x_dev} oracle {x_oracle} gap {gap:.3e} delta {delta:.3e}")
 
 
-def unpack_q4(packed: np.ndarray, scales_bits: np.ndarray, N: int, K: int):
+def unpack_q4(packed: np.ndarray, scales_bits: np.ndarray, N: int, K: int, fmt: str = "w4"):
     """Codes [N][K] (int8) and scales [N][K/128] (fp16 bits) from the
-    library's packed layout (documented in include/sd_api.h): for column
+    library's packed int4 layout (documented in include/sd_api.h): for column
     block nb = n/32 and group g, word (((nb*G + g)*2 + st//4)*64 + l)*4 + st%4
     of lane l = n%32 + 32*h holds codes k = 128g + 16st + 8h + e at nibble
-    4*(e//2) + 16*(e%2), stored as q + 8; scale (nb*G + g)*32 + n%32."""
+    4*(e//2) + 16*(e%2), stored as q + 8 ("w4") or q ("w4a"); scale
+    (nb*G + g)*32 + n%32."""
     G = K // 128
     words = packed.view(np.uint32).reshape(N // 32, G, 2, 64, 4)     # [nb, g, st//4, lane, st%4]
     codes = np.zeros((N, K), dtype=np.int8)
     lanes = np.arange(64)
     cols = (np.arange(N // 32)[:, None] * 32 + (lanes % 32)[None, :])  # [nb, lane]
     h = lanes // 32
+    off = 8 if fmt == "w4" else 0
     for st in range(8):
         w = words[:, :, st // 4, :, st % 4]                             # [nb, g, lane]
         for e in range(8):
-            nib = ((w >> np.uint32(4 * (e // 2) + 16 * (e % 2))) & np.uint32(15)).astype(np.int16) - 8
+            nib = ((w >> np.uint32(4 * (e // 2) + 16 * (e % 2))) & np.uint32(15)).astype(np.int16) - off
             for g in range(G):
                 ks = g * 128 + 16 * st + 8 * h + e                      # per lane
                 codes[cols, ks[None, :]] = nib[:, g, :]
-    sc = scales_bits.view(np.uint16).reshape(N // 32, G, 32).transpose(0, 2, 1).reshape(N, G)
-    return codes, sc
+    return codes, _unpack_groupwise(scales_bits.view(np.uint16), N, G)
 
 
-def drafter_layout(cfg: dict):
-    """(layer, which, N, K, code_offset, scale_offset) of every quantized
-    projection in the drafter buffer (include/sd_api.h)."""
+def unpack_q8(packed: np.ndarray, scales_bits: np.ndarray, N: int, K: int):
+    """Codes [N][K] (int8) and scales from the library's packed int8 layout:
+    code e of k-step st, lane l = n%32 + 32*h (k = 128g + 16st + 8h + e) is
+    byte e%4 of word j = 2*st + e//4 at index (((nb*G + g)*4 + j//4)*64 + l)*4
+    + j%4, stored as q + 128."""
+    G = K // 128
+    words = packed.view(np.uint32).reshape(N // 32, G, 4, 64, 4)     # [nb, g, j//4, lane, j%4]
+    codes = np.zeros((N, K), dtype=np.int8)
+    lanes = np.arange(64)
+    cols = (np.arange(N // 32)[:, None] * 32 + (lanes % 32)[None, :])
+    h = lanes // 32
+    for j in range(16):
+        w = words[:, :, j // 4, :, j % 4]
+        st = j // 2
+        for b in range(4):
+            e = 4 * (j % 2) + b
+            byte = ((w >> np.uint32(8 * b)) & np.uint32(255)).astype(np.int16) - 128
+            for g in range(G):
+                ks = g * 128 + 16 * st + 8 * h + e
+                codes[cols, ks[None, :]] = byte[:, g, :]
+    return codes, _unpack_groupwise(scales_bits.view(np.uint16), N, G)
+
+
+def _unpack_groupwise(x: np.ndarray, N: int, G: int):
+    """[N][G] from the per-(column, group) layout (nb*G + g)*32 + n%32."""
+    return x.reshape(N // 32, G, 32).transpose(0, 2, 1).reshape(N, G)
+
+
+def unpack_zeros(zero_bytes: np.ndarray, N: int, K: int):
+    return _unpack_groupwise(zero_bytes.view(np.uint8), N, K // 128)
+
+
+def drafter_layout(cfg: dict, fmt: str = "w4"):
+    """(layer, which, N, K, code_offset, scale_offset, zero_offset or None) of
+    every quantized projection in the drafter buffer (include/sd_api.h), and
+    the buffer's size."""
     H, d, F = cfg["hidden"], cfg["head_dim"], cfg["ffn"]
     shapes = [((cfg["n_q"] + 2 * cfg["n_kv"]) * d, H), (H, cfg["n_q"] * d), (2 * F, H), (H, F)]
     a256 = lambda x: (x + 255) // 256 * 256
     out, off = [], 0
     for l in range(cfg["n_layers"]):
         for w, (N, K) in enumerate(shapes):
-            cb, sb = a256(N * K // 2), a256(N * (K // 128) * 2)
-            out.append((l, w, N, K, off, off + cb))
-            off += cb + sb
+            cb = a256(N * K // (1 if fmt == "w8" else 2))
+            sb = a256(N * (K // 128) * 2)
+            zb = a256(N * (K // 128)) if fmt == "w4a" else 0
+            out.append((l, w, N, K, off, off + cb, off + cb + sb if zb else None))
+            off += cb + sb + zb
     return out, off

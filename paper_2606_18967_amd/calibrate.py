@@ -141,7 +141,7 @@ class Sweep:
     of (B, S, gamma).  KV context is random N(0, 1) (synth.fill_kv_context);
     kv_len is reset to S before each measurement."""
 
-    def __init__(self, cfg: dict, Bmax: int, Smax: int, gmax: int, seed: int = 2):
+    def __init__(self, cfg: dict, Bmax: int, Smax: int, gmax: int, seed: int = 2, fmt: str = "w4"):
         import torch
         self.torch = torch
         self.cfg = cfg
@@ -152,7 +152,7 @@ class Sweep:
         self.k, self.v, self.kv_len = self.eng.alloc_kv()
         self.eng.bind_kv(self.k, self.v, self.kv_len)
         synth.fill_kv_context(self.k, self.v, Smax, seed + 100)
-        self.eng.refresh_drafter()
+        self.qbuf = self.eng.refresh_drafter(fmt=fmt)
         self.seed = seed
         self.V = cfg["vocab"]
 
@@ -216,8 +216,38 @@ class Sweep:
         self.eng.sync()
         return emitted / (steps * B)
 
+    def set_drafter(self, fmt: str):
+        self.qbuf = self.eng.refresh_drafter(fmt=fmt)
+
     def close(self):
         self.eng.close()
+
+
+def drafter_tradeoff(cfg: dict, fmts=("w4", "w4a", "w8"), Bs=(1, 16, 64), S=2048, gamma=4, steps=10, reps=8,
+                     log=print):
+    """Latency against acceptance of the drafter formats (App. B.3, Table 4):
+    per format and batch, the measured T_q / T_p, the model's tau and alpha
+    at (B, S, gamma), and the SD speedup tau T_p / (gamma T_q + T_V) those
+    measurements give; next to them the cost model's idealized T_q / T_p
+    from bytes alone (weights at 16 bits, drafter projections at 4 or 8)."""
+    sw = Sweep(cfg, max(Bs), S, gamma)
+    rows = []
+    for fmt in fmts:
+        sw.set_drafter(fmt)
+        bits = 8.0 if fmt == "w8" else 4.0
+        ideal = sdrl.cost_init(cfg, drafter_bits=bits, BW_eff=1.0, F_eff=1e30)
+        for B in Bs:
+            r = sw.measure(B, S, [gamma], reps)
+            tau = sw.measured_tau(B, S, gamma, steps)
+            tp, tq, _ = sdrl.cost_times(ideal, B, S, gamma)
+            row = dict(fmt=fmt, B=B, S=S, gamma=gamma, T_p=r["p"], T_q=r["q"], T_V=r[("v", gamma)],
+                       tq_over_tp=r["q"] / r["p"], tq_over_tp_ideal=tq / tp, tau=tau,
+                       alpha=sdrl.alpha_from_tau(min(tau, gamma + 1 - 1e-9), gamma),
+                       speedup=tau * r["p"] / (gamma * r["q"] + r[("v", gamma)]))
+            log(json.dumps(row))
+            rows.append(row)
+    sw.close()
+    return rows
 
 
 def run(cfg: dict, Bs, Ss, gammas, taus, eps=0.05, reps=8, log=print):
@@ -259,9 +289,20 @@ def main(argv=None):
     ap.add_argument("--eps", type=float, default=0.05)
     ap.add_argument("--reps", type=int, default=8)
     ap.add_argument("--out", default="")
+    ap.add_argument("--drafter-tradeoff", action="store_true",
+                    help="only compare the drafter formats (latency against acceptance) at S = max(--S)")
     a = ap.parse_args(argv)
     cfg = synth.L4_8B if a.model == "L4_8B" else dict(synth.TINY, dtype="bf16", name="tiny-bf16")
     ints = lambda s: [int(x) for x in s.split(",") if x]
+    if a.drafter_tradeoff:
+        rows = drafter_tradeoff(cfg, Bs=ints(a.B), S=max(ints(a.S)), gamma=max(ints(a.gamma)), reps=a.reps,
+                                log=lambda *x: print(*x, file=sys.stderr, flush=True))
+        txt = json.dumps(rows, indent=1)
+        if a.out:
+            with open(a.out, "w") as fh:
+                fh.write(txt)
+        print(txt)
+        return
     res = run(cfg, ints(a.B), ints(a.S), ints(a.gamma), [float(x) for x in a.tau.split(",")], a.eps, a.reps,
               log=lambda *x: print(*x, file=sys.stderr, flush=True))
     txt = json.dumps(res, indent=1, default=str)

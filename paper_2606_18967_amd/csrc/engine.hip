@@ -61,6 +61,8 @@ struct sd_engine_s {
     int32_t* kv_len = nullptr;
     std::vector<const uint32_t*> qw;   // [L*4] packed codes
     std::vector<const uint16_t*> qs;   // [L*4] scales
+    std::vector<const uint8_t*> qz;    // [L*4] zero points (asymmetric format), else NULL
+    int qfmt = QF_W4;                  // format of the last refresh
     bool drafter_ready = false;
     // workspace (engine-owned)
     float* h = nullptr;
@@ -128,13 +130,17 @@ static void prj_shape(const sd_model_cfg& c, int which, int* N, int* K)
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static size_t prj_bytes(const sd_model_cfg& c, int which, size_t* codes, size_t* scales)
+// bytes of one quantized projection in format fmt: codes, fp16 scales and
+// (asymmetric format) one zero-point byte per (column, group), each block
+// 256-byte aligned
+static size_t prj_bytes(const sd_model_cfg& c, int which, int fmt, size_t* codes, size_t* scales, size_t* zeros)
 {
     int N, K;
     prj_shape(c, which, &N, &K);
-    *codes = align256((size_t)N * K / 2);
+    *codes = align256(qfmt_code_bytes(fmt, N, K));
     *scales = align256((size_t)N * (K / 128) * 2);
-    return *codes + *scales;
+    *zeros = fmt == QF_W4A ? align256((size_t)N * (K / 128)) : 0;
+    return *codes + *scales + *zeros;
 }
 
 static sd_status check_cfg(const sd_model_cfg* c)
@@ -165,13 +171,15 @@ extern "C" size_t sd_kv_bytes(const sd_model_cfg* c, int32_t max_slots, int32_t 
     return (size_t)c->n_layers * max_slots * c->n_kv * (size_t)max_ctx * c->head_dim * el;
 }
 
-extern "C" size_t sd_drafter_bytes(const sd_model_cfg* c)
+extern "C" size_t sd_drafter_bytes_fmt(const sd_model_cfg* c, int32_t fmt)
 {
-    if (!c) return 0;
-    size_t total = 0, a, b;
-    for (int w = 0; w < 4; ++w) total += prj_bytes(*c, w, &a, &b);
+    if (!c || fmt < SD_DRAFT_W4 || fmt > SD_DRAFT_W8) return 0;
+    size_t total = 0, a, b, z;
+    for (int w = 0; w < 4; ++w) total += prj_bytes(*c, w, fmt, &a, &b, &z);
     return total * (size_t)c->n_layers;
 }
+
+extern "C" size_t sd_drafter_bytes(const sd_model_cfg* c) { return sd_drafter_bytes_fmt(c, SD_DRAFT_W4); }
 
 // Largest split-K scratch any projection or the LM head needs for up to R rows.
 static size_t gpart_bytes(const sd_model_cfg& c, int R)
@@ -229,6 +237,7 @@ extern "C" sd_status sd_create(const sd_model_cfg* cfg, int32_t max_slots, int32
     e->w.assign(sd_num_weights(cfg), nullptr);
     e->qw.assign(4 * cfg->n_layers, nullptr);
     e->qs.assign(4 * cfg->n_layers, nullptr);
+    e->qz.assign(4 * cfg->n_layers, nullptr);
     if (hipGetDevice(&e->dev) != hipSuccess) { delete e; return fail(SD_E_HIP, "hipGetDevice failed"); }
 
     const sd_model_cfg& c = *cfg;
@@ -316,30 +325,44 @@ extern "C" sd_status sd_set_debug(sd_engine e, int32_t poison)
 
 static const void* W(sd_engine e, int layer, int idx) { return e->w[3 + 6 * layer + idx]; }
 
-extern "C" sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream)
+extern "C" sd_status sd_refresh_drafter_fmt(sd_engine e, int32_t fmt, void* qbuf, size_t bytes, void* stream)
 {
     if (!e || !qbuf) return fail(SD_E_INVAL, "NULL argument");
+    if (fmt < SD_DRAFT_W4 || fmt > SD_DRAFT_W8) return fail(SD_E_INVAL, "unknown drafter format %d", fmt);
+    if (((uintptr_t)qbuf) & 15) return fail(SD_E_INVAL, "qbuf must be 16-byte aligned");
     if (!e->weights_bound) return fail(SD_E_STATE, "weights not bound");
-    if (bytes < sd_drafter_bytes(&e->c)) return fail(SD_E_INVAL, "qbuf holds %zu bytes, need %zu", bytes, sd_drafter_bytes(&e->c));
+    const size_t need = sd_drafter_bytes_fmt(&e->c, fmt);
+    if (bytes < need) return fail(SD_E_INVAL, "qbuf holds %zu bytes, need %zu", bytes, need);
+    e->drafter_ready = false;
     hipStream_t s = (hipStream_t)stream;
     char* p = (char*)qbuf;
     static const int widx[4] = {1, 2, 4, 5};   // Wqkv, Wo, Wgu, Wdown within a layer
     for (int l = 0; l < e->c.n_layers; ++l)
         for (int wh = 0; wh < 4; ++wh) {
             int N, K;
-            size_t cb, sb;
+            size_t cb, sb, zb;
             prj_shape(e->c, wh, &N, &K);
-            prj_bytes(e->c, wh, &cb, &sb);
+            prj_bytes(e->c, wh, fmt, &cb, &sb, &zb);
             uint32_t* q = (uint32_t*)p;
             uint16_t* sc = (uint16_t*)(p + cb);
-            launch_quant_rtn4(W(e, l, widx[wh]), e->f32, N, K, q, sc, s);
+            uint8_t* z = zb ? (uint8_t*)(p + cb + sb) : nullptr;
+            launch_quant(fmt, W(e, l, widx[wh]), e->f32, N, K, q, sc, z, s);
             e->qw[4 * l + wh] = q;
             e->qs[4 * l + wh] = sc;
-            p += cb + sb;
+            e->qz[4 * l + wh] = z;
+            p += cb + sb + zb;
         }
     sd_status st = launched("sd_refresh_drafter");
-    if (st == SD_OK) e->drafter_ready = true;
+    if (st == SD_OK) {
+        e->qfmt = fmt;
+        e->drafter_ready = true;
+    }
     return st;
+}
+
+extern "C" sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream)
+{
+    return sd_refresh_drafter_fmt(e, SD_DRAFT_W4, qbuf, bytes, stream);
 }
 
 // ------------------------------------------------------------------ forward
@@ -356,8 +379,10 @@ static int proj(sd_engine e, bool draft, int layer, int which, const void* A, fl
     if (draft) {
         const uint32_t* q = e->qw[4 * layer + which];
         const uint16_t* sc = e->qs[4 * layer + which];
-        if (e->f32) { launch_gemm_q4_f32((const float*)A, q, sc, C, M, N, K, ldc, mode, s); return 1; }
-        const int S = launch_gemm_q4((const uint16_t*)A, q, sc, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, s);
+        const uint8_t* z = e->qz[4 * layer + which];
+        if (e->f32) { launch_gemm_q4_f32((const float*)A, q, sc, z, e->qfmt, C, M, N, K, ldc, mode, s); return 1; }
+        const int S = launch_gemm_q4((const uint16_t*)A, q, sc, z, e->qfmt, C, e->gpart, e->gpart_cap, M, N, K, ldc,
+                                     mode, s);
         if (S < 1) e->launch_err = 1;   // cannot happen for a configuration check_cfg accepted
         return S < 1 ? 1 : S;
     }

@@ -62,23 +62,33 @@ enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
 int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part, size_t part_cap, int M, int N, int K,
                      int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s);
 size_t gemm_part_floats(int M, int N, int K);
-// ---- int4 drafter GEMM (kernels_q4.hip): C[M][N] (+)= A[M][K] Wq^T, A fp16,
-// Wq in the packed 32-column tile layout, N % 32 == 0.  Returns the number of
-// K splits S (partials left in part as [S][M][N] when S > 1, for the consumer
-// to sum), or -1 for an unsupported shape or a too small part.
-int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, float* C, float* part, size_t part_cap,
-                   int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+// ---- drafter weight formats: RTN over groups of 128 weights along K, one
+// fp16 scale per (column, group); int4 symmetric (codes stored as q + 8),
+// int4 asymmetric (codes q in 0..15 plus a zero point z per (column,
+// group), w = s (q - z)) and int8 symmetric (codes stored as q + 128).
+enum qfmt : int { QF_W4 = 0, QF_W4A = 1, QF_W8 = 2 };
+// bytes of the packed codes of an [N][K] matrix
+inline size_t qfmt_code_bytes(int fmt, int N, int K) { return (size_t)N * K / (fmt == QF_W8 ? 1 : 2); }
+
+// ---- quantized drafter GEMM (kernels_q4.hip): C[M][N] (+)= A[M][K] Wq^T,
+// A fp16, Wq in the packed 32-column tile layout of format fmt, Z the zero
+// points (QF_W4A only), N % 32 == 0.  Returns the number of K splits S
+// (partials left in part as [S][M][N] when S > 1, for the consumer to sum),
+// or -1 for an unsupported shape or a too small part.
+int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt, float* C,
+                   float* part, size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
 size_t gemm_q4_part_floats(int M, int N, int K);
-// 1 if the int4 GEMM supports reduction length K.
+// 1 if the quantized GEMM supports reduction length K.
 int gemm_q4_k_ok(int K);
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc,
                      gemm_mode mode, hipStream_t s);
-void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M,
-                        int N, int K, int ldc, gemm_mode mode, hipStream_t s);
+void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt, float* C,
+                        int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s);
 
-// ---- RTN quantizer (kernels_quant.hip)
-void launch_quant_rtn4(const void* W, int w_f32, int N, int K, uint32_t* Wq, uint16_t* Sc,
-                       hipStream_t s);
+// ---- RTN quantizer (kernels_quant.hip): W [N][K] (fp32 or bf16) into the
+// packed layout of format fmt, scales Sc and (QF_W4A) zero points Z
+void launch_quant(int fmt, const void* W, int w_f32, int N, int K, uint32_t* Wq, uint16_t* Sc, uint8_t* Z,
+                  hipStream_t s);
 
 // ---- sampling and acceptance (kernels_sample.hip)
 struct rng_t { uint64_t seed, step; };

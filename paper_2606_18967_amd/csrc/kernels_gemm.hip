@@ -450,18 +450,26 @@ __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__
 
 // ------------------------------------------------------------------ int4 x fp32 VALU
 // code of weight (n, k) in the packed layout of kernels_q4.hip
-__device__ __forceinline__ int q4_code(const uint32_t* Wq, int G, int n, int k)
+// the stored code of weight (n, k) in the packed layout of format fmt
+// (kernels_q4.hip), before the zero point is taken off
+__device__ __forceinline__ int q_stored(const uint32_t* Wq, int fmt, int G, int n, int k)
 {
     const int nb = n >> 5, g = k >> 7, kk = k & 127;
     const int st = kk >> 4, h = (kk >> 3) & 1, e = kk & 7;
     const int l = (n & 31) + 32 * h;
+    if (fmt == QF_W8) {
+        const int j = 2 * st + (e >> 2);
+        const uint32_t word = Wq[((((size_t)nb * G + g) * 4 + (j >> 2)) * 64 + l) * 4 + (j & 3)];
+        return (int)((word >> (8 * (e & 3))) & 255u);
+    }
     const uint32_t word = Wq[((((size_t)nb * G + g) * 2 + (st >> 2)) * 64 + l) * 4 + (st & 3)];
-    return (int)((word >> (4 * (e >> 1) + 16 * (e & 1))) & 15u) - 8;
+    return (int)((word >> (4 * (e >> 1) + 16 * (e & 1))) & 15u);
 }
 
 __global__ void __launch_bounds__(256) k_gemm_q4_f32(const float* __restrict__ A, const uint32_t* __restrict__ Wq,
-                                                     const uint16_t* __restrict__ Sc, float* __restrict__ C, int M,
-                                                     int N, int K, int ldc, int mode)
+                                                     const uint16_t* __restrict__ Sc, const uint8_t* __restrict__ Z,
+                                                     int fmt, float* __restrict__ C, int M, int N, int K, int ldc,
+                                                     int mode)
 {
     int n = blockIdx.x * 64 + (threadIdx.x & 63);
     int m = blockIdx.y * 4 + (threadIdx.x >> 6);
@@ -470,9 +478,11 @@ __global__ void __launch_bounds__(256) k_gemm_q4_f32(const float* __restrict__ A
     const float* ar = A + (size_t)m * K;
     float acc = 0.f;
     for (int g = 0; g < G; ++g) {
+        const size_t si = ((size_t)(n >> 5) * G + g) * 32 + (n & 31);
+        const int z = fmt == QF_W8 ? 128 : (fmt == QF_W4A ? (int)Z[si] : 8);
         float part = 0.f;
-        for (int k = g * 128; k < g * 128 + 128; ++k) part += ar[k] * (float)q4_code(Wq, G, n, k);
-        acc += f16_bits_to_f32(Sc[((size_t)(n >> 5) * G + g) * 32 + (n & 31)]) * part;
+        for (int k = g * 128; k < g * 128 + 128; ++k) part += ar[k] * (float)(q_stored(Wq, fmt, G, n, k) - z);
+        acc += f16_bits_to_f32(Sc[si]) * part;
     }
     float* cp = C + (size_t)m * ldc + n;
     *cp = mode == GEMM_ADD ? *cp + acc : acc;
@@ -596,9 +606,9 @@ void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int
     k_gemm_f32<<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, mode);
 }
 
-void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, float* C, int M, int N, int K,
-                        int ldc, gemm_mode mode, hipStream_t s)
+void launch_gemm_q4_f32(const float* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt, float* C,
+                        int M, int N, int K, int ldc, gemm_mode mode, hipStream_t s)
 {
     dim3 grid((N + 63) / 64, (M + 3) / 4);
-    k_gemm_q4_f32<<<grid, 256, 0, s>>>(A, Wq, Sc, C, M, N, K, ldc, mode);
+    k_gemm_q4_f32<<<grid, 256, 0, s>>>(A, Wq, Sc, Z, fmt, C, M, N, K, ldc, mode);
 }

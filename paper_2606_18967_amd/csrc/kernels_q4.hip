@@ -1,25 +1,34 @@
-// kernels_q4.hip -- the drafter's W4A16 projections: C[M][N] (+)= A[M][K] Wq^T
-// with A in fp16, int4 group-128 weights with one fp16 scale per (column,
-// group) (Sec. 4.1), fp32 accumulation.  Drafting runs one token per
-// sequence, so M is the live batch (64 in the 8B-shaped workload) and the
-// weights are streamed from HBM exactly once per m-tile of 64 rows.
+// kernels_q4.hip -- the drafter's weight-only quantized projections:
+// C[M][N] (+)= A[M][K] Wq^T with A in fp16, RTN weights in groups of 128
+// along K with one fp16 scale per (column, group) (Sec. 4.1), fp32
+// accumulation.  Formats: int4 symmetric (the default), int4 asymmetric with
+// a zero point per (column, group) (App. B.2) and int8 symmetric (the W8
+// drafter of App. B.3).  Drafting runs one token per sequence, so M is the
+// live batch (64 in the 8B-shaped workload) and the weights are streamed
+// from HBM exactly once per m-tile of 64 rows.
 //
-// Packed weight layout (written by the drafter refresh): for column block
+// Packed int4 layout (written by the drafter refresh): for column block
 // nb = n / 32 and group g = k / 128 of a [N][K] matrix, G = K / 128, lane
 // l in 0..63 stands for column 32 nb + (l & 31) and k-half h = l >> 5.  For
 // k-step s in 0..7 (16 k each) lane l owns the uint32 word with the 8 codes
 // k = 128 g + 16 s + 8 h + e, e = 0..7; code e sits in the nibble at bit
-// 4 (e / 2) + 16 (e % 2), stored as q + 8.  The word of (nb, g, l, s) is at
-// index (((nb G + g) 2 + s / 4) 64 + l) 4 + s % 4, so each wave reads one
-// group of its block with two fully contiguous 1 KB loads.  The scale of
-// column n, group g is at (nb G + g) 32 + n % 32.
+// 4 (e / 2) + 16 (e % 2), stored as q + 8 (symmetric) or q (asymmetric).
+// The word of (nb, g, l, s) is at index (((nb G + g) 2 + s / 4) 64 + l) 4 +
+// s % 4, so each wave reads one group of its block with two fully contiguous
+// 1 KB loads.  The int8 layout has two words per k-step: code e of k-step s
+// is byte e % 4 of word j = 2 s + e / 4, stored as q + 128, at index
+// (((nb G + g) 4 + j / 4) 64 + l) 4 + j % 4 (four 1 KB loads per group).
+// Scale and zero point of column n, group g are at (nb G + g) 32 + n % 32.
 //
-// That word is exactly lane l's B operand of v_mfma_f32_32x32x16_f16 for
-// k-step s (column l & 31, k 8 h .. 8 h + 7 of the step).  Dequantization
-// uses the fp16 pattern 0x6400 = 1024: OR-ing a nibble into mantissa bits
-// 0..3 gives 1024 + (q + 8) and into bits 4..7 gives 1024 + 16 (q + 8), so
-// a subtract of 1032, or a fused multiply by 1/16 and add of -72, leaves the
-// code q exactly.  The group's partial product is scaled in fp32.
+// Those words are exactly lane l's B operand of v_mfma_f32_32x32x16_f16
+// for k-step s (column l & 31, k 8 h .. 8 h + 7 of the step).
+// Dequantization uses the fp16 pattern 0x6400 = 1024: OR-ing a nibble into
+// mantissa bits 0..3 gives 1024 + c and into bits 4..7 gives 1024 + 16 c
+// for the stored code c, so a subtract of 1024 + z (z = 8 symmetric, the
+// group's zero point asymmetric), or a fused multiply by 1/16 and add of
+// -(64 + z), leaves q - z exactly; an int8 code is placed in the low byte
+// of an fp16 1024 by a byte permute and 1152 subtracted.  The group's
+// partial product is scaled in fp32.
 //
 // Work-group: 8 waves = 4 column blocks (128 columns) x 2 k-halves.  Waves
 // of k-half hh take the groups g0 + hh, g0 + hh + 2, ... of the split, so
@@ -52,32 +61,45 @@ __device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t o
     return r;
 }
 
-// lane's B operand for one k-step from its packed word; lo / hi are the
+// lane's B operand for one k-step from its packed int4 word; lo / hi are the
 // nibble masks 0x000F000F / 0x00F000F0 and magic the fp16 pair 1024, 1024,
-// passed in registers
-__device__ __forceinline__ half8 dq_word(uint32_t w, uint32_t lo, uint32_t hi, uint32_t magic)
+// passed in registers; sub = 1024 + z and mhi = -(64 + z) as fp16 pairs
+__device__ __forceinline__ half8 dq_word(uint32_t w, uint32_t lo, uint32_t hi, uint32_t magic, half2v sub, half2v mhi)
 {
-    const half2v sub = {(_Float16)1032.0f, (_Float16)1032.0f};
     const half2v sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
-    const half2v m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
     const uint32_t w2 = w >> 8;
     const half2v p0 = __builtin_bit_cast(half2v, and_or(w, lo, magic)) - sub;
-    const half2v p1 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, and_or(w, hi, magic)), sixteenth, m72);
+    const half2v p1 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, and_or(w, hi, magic)), sixteenth, mhi);
     const half2v p2 = __builtin_bit_cast(half2v, and_or(w2, lo, magic)) - sub;
-    const half2v p3 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, and_or(w2, hi, magic)), sixteenth, m72);
+    const half2v p3 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, and_or(w2, hi, magic)), sixteenth, mhi);
     return (half8){p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
-template <int MT, int D>
+// the same for the int8 format: codes 0..3 of w0, then of w1; magic holds
+// 0x64 in every byte, so each permute builds the fp16 pair 1024 + c0, 1024 + c1
+__device__ __forceinline__ half8 dq_bytes(uint32_t w0, uint32_t w1, uint32_t magic)
+{
+    const half2v sub = {(_Float16)1152.0f, (_Float16)1152.0f};
+    const half2v p0 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(magic, w0, 0x04010400u)) - sub;
+    const half2v p1 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(magic, w0, 0x04030402u)) - sub;
+    const half2v p2 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(magic, w1, 0x04010400u)) - sub;
+    const half2v p3 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(magic, w1, 0x04030402u)) - sub;
+    return (half8){p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
+}
+
+template <int MT, int D, int FMT>
 __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A, const uint32_t* __restrict__ Wq,
-                                                 const uint16_t* __restrict__ Sc, float* __restrict__ C,
+                                                 const uint16_t* __restrict__ Sc, const uint8_t* __restrict__ Zp,
+                                                 float* __restrict__ C,
                                                  float* __restrict__ P, int M, int N, int K, int ldc, int mode,
                                                  int S, int msup, int total)
 {
     constexpr int ROWS = 32 * MT;                      // rows of one m-tile
     constexpr int AP = ROWS * 2 * (QK / 8) / 512;      // 16-byte A pieces per thread per iteration
+    constexpr int WPL = FMT == QF_W8 ? 4 : 2;          // 16-byte weight pieces per lane per group
     __shared__ __attribute__((aligned(16))) uint16_t As[2][2][ROWS * QLD];
     __shared__ __attribute__((aligned(16))) uint16_t Ss[4 * QSMAX * 32];
+    __shared__ __attribute__((aligned(16))) uint8_t Zs[FMT == QF_W4A ? 4 * QSMAX * 32 : 16];
 
     const int per_xcd = gridDim.x >> 3;                // gridDim.x is a multiple of 8
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
@@ -102,6 +124,11 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
     const int sidx = min(tid, 16 * Gs - 1);
     const int sb = sidx / (Gs * 4), sr = sidx - sb * (Gs * 4);
     const u32x4 sv = *(const u32x4*)(Sc + ((size_t)min(tile * 4 + sb, nblk - 1) * G + g0) * 32 + sr * 8);
+    // zero points (asymmetric format): 4 runs of Gs*32 bytes, one 16-byte piece per thread
+    const int zidx = min(tid, 8 * Gs - 1);
+    const int zb = zidx / (Gs * 2), zr = zidx - zb * (Gs * 2);
+    u32x4 zv = {0u, 0u, 0u, 0u};
+    if (FMT == QF_W4A) zv = *(const u32x4*)(Zp + ((size_t)min(tile * 4 + zb, nblk - 1) * G + g0) * 32 + zr * 16);
 
     // A pieces: p = tid + 512 t -> (half, row, 16-byte column)
     u32x4 ar[D][AP];
@@ -124,12 +151,12 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
             *(u32x4*)&As[buf][half][row * QLD + col] = a[t];
         }
     };
-    u32x4 wr[D][2];
-    auto load_w = [&](int it, u32x4 (&q)[2]) {
+    u32x4 wr[D][WPL];
+    auto load_w = [&](int it, u32x4 (&q)[WPL]) {
         const int g = min(g0 + 2 * it + hh, g1 - 1);
-        const u32x4* base = (const u32x4*)Wq + ((size_t)nbl * G + g) * 128;
-        q[0] = base[lane];
-        q[1] = base[64 + lane];
+        const u32x4* base = (const u32x4*)Wq + ((size_t)nbl * G + g) * (64 * WPL);
+#pragma unroll
+        for (int i = 0; i < WPL; ++i) q[i] = base[64 * i + lane];
     };
 
     floatx16 acc[MT];
@@ -138,14 +165,23 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
 
-    uint32_t lo = 0x000F000Fu, hi = 0x00F000F0u, magic = 0x64006400u;
+    uint32_t lo = 0x000F000Fu, hi = 0x00F000F0u, magic = FMT == QF_W8 ? 0x64646464u : 0x64006400u;
     asm volatile("" : "+v"(lo), "+v"(hi), "+v"(magic));   // keep the constants in VGPRs
-    auto compute = [&](int buf, int it, const u32x4 (&q)[2]) {
+    auto compute = [&](int buf, int it, const u32x4 (&q)[WPL]) {
         const uint16_t* ab = &As[buf][hh][(lane & 31) * QLD + 8 * (lane >> 5)];
+        const int gi = 2 * it + hh;
+        half2v sub = {(_Float16)1032.0f, (_Float16)1032.0f}, mhi = {(_Float16)-72.0f, (_Float16)-72.0f};
+        if (FMT == QF_W4A) {
+            const _Float16 z = (_Float16)(float)Zs[cb * QSMAX * 32 + min(gi, Gs - 1) * 32 + (lane & 31)];
+            sub = (half2v){(_Float16)1024.0f + z, (_Float16)1024.0f + z};
+            mhi = (half2v){(_Float16)-64.0f - z, (_Float16)-64.0f - z};
+        }
         floatx16 tmp[MT];
 #pragma unroll
         for (int st = 0; st < 8; ++st) {
-            const half8 b = dq_word(q[st >> 2][st & 3], lo, hi, magic);
+            half8 b;
+            if (FMT == QF_W8) b = dq_bytes(q[st >> 1][2 * (st & 1)], q[st >> 1][2 * (st & 1) + 1], magic);
+            else b = dq_word(q[st >> 2][st & 3], lo, hi, magic, sub, mhi);
 #pragma unroll
             for (int t = 0; t < MT; ++t) {
                 const half8 a = *(const half8*)(ab + t * 32 * QLD + 16 * st);
@@ -160,7 +196,6 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
             }
         }
         // a padding group (past the split) contributes nothing
-        const int gi = 2 * it + hh;
         const float sv_ = h2f(Ss[cb * QSMAX * 32 + min(gi, Gs - 1) * 32 + (lane & 31)]);
         const float sc = gi < Gs ? sv_ : 0.f;
 #pragma unroll
@@ -176,6 +211,7 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
         load_w(min(u, nit - 1), wr[u]);
     }
     if (tid < 16 * Gs) *(u32x4*)&Ss[sb * QSMAX * 32 + sr * 8] = sv;
+    if (FMT == QF_W4A && tid < 8 * Gs) *(u32x4*)&Zs[zb * QSMAX * 32 + zr * 16] = zv;
     store_a(0, ar[0]);
     lds_barrier();
 
@@ -245,13 +281,24 @@ int q4_plan(int M, int N, int K)
     return best;
 }
 
-template <int MT>
-void q4_launch_d(int D, dim3 grid, hipStream_t st, const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, float* C,
-                 float* P, int M, int N, int K, int ldc, int mode, int S, int msup, int total)
+template <int MT, int FMT>
+void q4_launch_d(int D, dim3 grid, hipStream_t st, const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc,
+                 const uint8_t* Z, float* C, float* P, int M, int N, int K, int ldc, int mode, int S, int msup,
+                 int total)
 {
-    if (D == 2) k_gemm_q4<MT, 2><<<grid, 512, 0, st>>>(A, Wq, Sc, C, P, M, N, K, ldc, mode, S, msup, total);
-    else if (D == 3) k_gemm_q4<MT, 3><<<grid, 512, 0, st>>>(A, Wq, Sc, C, P, M, N, K, ldc, mode, S, msup, total);
-    else k_gemm_q4<MT, 4><<<grid, 512, 0, st>>>(A, Wq, Sc, C, P, M, N, K, ldc, mode, S, msup, total);
+    if (D == 2) k_gemm_q4<MT, 2, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    else if (D == 3) k_gemm_q4<MT, 3, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    else k_gemm_q4<MT, 4, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+}
+
+template <int MT>
+void q4_launch_f(int fmt, int D, dim3 grid, hipStream_t st, const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc,
+                 const uint8_t* Z, float* C, float* P, int M, int N, int K, int ldc, int mode, int S, int msup,
+                 int total)
+{
+    if (fmt == QF_W4A) q4_launch_d<MT, QF_W4A>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    else if (fmt == QF_W8) q4_launch_d<MT, QF_W8>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    else q4_launch_d<MT, QF_W4>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
 }
 
 }  // namespace
@@ -264,10 +311,10 @@ size_t gemm_q4_part_floats(int M, int N, int K)
     return S > 1 ? (size_t)S * M * N : 0;
 }
 
-int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, float* C, float* part, size_t part_cap,
-                   int M, int N, int K, int ldc, gemm_mode mode, hipStream_t st)
+int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt, float* C,
+                   float* part, size_t part_cap, int M, int N, int K, int ldc, gemm_mode mode, hipStream_t st)
 {
-    if (K % QK || N % 32 || M < 1) return -1;
+    if (K % QK || N % 32 || M < 1 || fmt < QF_W4 || fmt > QF_W8 || (fmt == QF_W4A && !Z)) return -1;
     const int S = q4_plan(M, N, K);
     if (S < 1 || (S > 1 && (size_t)S * M * N > part_cap)) return -1;
     const int G = K / QK, nit = (G / S + 1) / 2;
@@ -277,7 +324,7 @@ int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, fl
     const int msup = (M + 63) / 64;
     const int total = (N / 32 + 3) / 4 * S * msup;
     dim3 grid((total + 7) / 8 * 8);
-    if (M <= 32) q4_launch_d<1>(D, grid, st, A, Wq, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
-    else q4_launch_d<2>(D, grid, st, A, Wq, Sc, C, part, M, N, K, ldc, mode, S, msup, total);
+    if (M <= 32) q4_launch_f<1>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
+    else q4_launch_f<2>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
     return S;
 }

@@ -27,14 +27,18 @@ SD_DTYPE_F32, SD_DTYPE_BF16 = 0, 1
 # The names every build must export (one per declaration in include/sd_api.h).
 API_SYMBOLS = (
     "sd_last_error", "sd_create", "sd_destroy", "sd_num_weights", "sd_bind_weights", "sd_kv_bytes",
-    "sd_bind_kv", "sd_drafter_bytes", "sd_refresh_drafter", "sd_prefill", "sd_draft", "sd_verify",
+    "sd_bind_kv", "sd_drafter_bytes", "sd_drafter_bytes_fmt", "sd_refresh_drafter", "sd_refresh_drafter_fmt",
+    "sd_prefill", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
     "sd_alpha_from_tau", "sd_timing", "sd_timing_read", "sd_dense_gemm_bf16",
 )
 
 # kernel classes of sd_timing_read
-T_ATTN, T_Q4, T_PROJ, T_LMHEAD, T_SAMPLE, T_ACCEPT, T_MISC = range(7)
+T_ATTN_D, T_ATTN_V, T_Q4, T_PROJ, T_LMHEAD, T_SAMPLE, T_ACCEPT, T_MISC = range(8)
+
+# drafter weight formats (sd_draft_fmt): int4 symmetric, int4 asymmetric, int8
+DRAFT_FORMATS = {"w4": 0, "w4a": 1, "w8": 2}
 T_NAMES = ("attn_decode", "attn_verify", "int4_proj", "bf16_proj", "lm_head", "sampler", "accept", "misc")
 
 
@@ -87,6 +91,8 @@ def lib():
             "sd_bind_kv": (_i32, [_P, _P, _P, _P]),
             "sd_drafter_bytes": (_sz, [_P]),
             "sd_refresh_drafter": (_i32, [_P, _P, _sz, _P]),
+            "sd_drafter_bytes_fmt": (_sz, [_P, _i32]),
+            "sd_refresh_drafter_fmt": (_i32, [_P, _i32, _P, _sz, _P]),
             "sd_prefill": (_i32, [_P, _i32, _P, _P, _i32, _P]),
             "sd_draft": (_i32, [_P, _i32, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
             "sd_verify": (_i32, [_P, _i32, _P, _P, _P, _i32, _P, _P]),
@@ -207,18 +213,21 @@ class Engine:
                                 _dev(kv_len, "kv_len", torch.int32, (self.max_slots,), self.device)))
         self._keep_kv = (k, v, kv_len)
 
-    def drafter_bytes(self) -> int:
-        return int(lib().sd_drafter_bytes(C.byref(self.c)))
+    def drafter_bytes(self, fmt: str = "w4") -> int:
+        return int(lib().sd_drafter_bytes_fmt(C.byref(self.c), DRAFT_FORMATS[fmt]))
 
-    def refresh_drafter(self, qbuf: torch.Tensor | None = None) -> torch.Tensor:
-        n = self.drafter_bytes()
+    def refresh_drafter(self, qbuf: torch.Tensor | None = None, fmt: str = "w4") -> torch.Tensor:
+        """RTN-quantizes the bound target into the drafter (format "w4", "w4a"
+        or "w8"); returns the caller-owned buffer the drafter reads."""
+        n = self.drafter_bytes(fmt)
         if qbuf is None:
             qbuf = torch.empty(n, dtype=torch.uint8, device=self.device)
         if qbuf.numel() * qbuf.element_size() < n:
             raise ValueError("qbuf too small")
-        _check(lib().sd_refresh_drafter(self.h, _dev(qbuf, "qbuf", None, None, self.device),
-                                        qbuf.numel() * qbuf.element_size(), _stream()))
+        _check(lib().sd_refresh_drafter_fmt(self.h, DRAFT_FORMATS[fmt], _dev(qbuf, "qbuf", None, None, self.device),
+                                            qbuf.numel() * qbuf.element_size(), _stream()))
         self._keep_q = qbuf
+        self.drafter_fmt = fmt
         return qbuf
 
     def set_debug(self, poison: bool):

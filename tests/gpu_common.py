@@ -20,19 +20,19 @@ def host_bits(tensors):
     return [synth.to_numpy_bits(t) for t in tensors]
 
 
-def oracle_models(cfg, W_host):
+def oracle_models(cfg, W_host, fmt="w4"):
     kind = oracle.BF16 if cfg["dtype"] == "bf16" else oracle.F32
     target = oracle.Model(cfg, W_host, kind)
-    drafter = oracle.make_drafter(cfg, W_host, kind)
+    drafter = oracle.make_drafter(cfg, W_host, kind, fmt=fmt)
     return target, drafter
 
 
-def make_engine(cfg, W_dev, max_slots, max_ctx, max_gamma):
+def make_engine(cfg, W_dev, max_slots, max_ctx, max_gamma, fmt="w4"):
     eng = sdrl.Engine(cfg, max_slots, max_ctx, max_gamma)
     eng.bind_weights(W_dev)
     k, v, kv_len = eng.alloc_kv()
     eng.bind_kv(k, v, kv_len)
-    eng.refresh_drafter()
+    eng.refresh_drafter(fmt=fmt)
     return eng, k, v, kv_len
 
 

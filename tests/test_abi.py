@@ -82,3 +82,10 @@ def test_sizes():
     from oracle.parity import drafter_layout
     _, total = drafter_layout(synth.L4_8B)
     assert L.sd_drafter_bytes(C.byref(c)) == total
+    for fmt, code in sdrl.DRAFT_FORMATS.items():
+        _, total = drafter_layout(synth.L4_8B, fmt)
+        assert L.sd_drafter_bytes_fmt(C.byref(c), code) == total, fmt
+    assert L.sd_drafter_bytes_fmt(C.byref(c), 3) == 0
+    assert L.sd_drafter_bytes_fmt(C.byref(c), -1) == 0
+    # host-side argument checks of the refresh need no device
+    assert L.sd_refresh_drafter_fmt(None, 1, None, 0, None) == 1      # SD_E_INVAL

@@ -22,14 +22,14 @@ from gpu_common import host_bits, host_bufs, i32, make_engine, oracle_kv_from_de
 pytestmark = pytest.mark.gpu
 
 
-def run_rollout(cfg, W, prompt, B, ctx_target, gamma, T, seed, step, tol, ctx_fill=0, n_steps=None):
+def run_rollout(cfg, W, prompt, B, ctx_target, gamma, T, seed, step, tol, ctx_fill=0, n_steps=None, fmt="w4"):
     """Grows B sequences with SD on the device and the oracle side by side."""
     P = prompt.shape[1]
     cap = ctx_fill + ctx_target + gamma + 2
     Wd = [w.cuda() for w in W]
-    eng, k, v, kv_len = make_engine(cfg, Wd, B, cap, gamma)
+    eng, k, v, kv_len = make_engine(cfg, Wd, B, cap, gamma, fmt)
     Wh = host_bits(W)
-    target, drafter = oracle_models(cfg, Wh)
+    target, drafter = oracle_models(cfg, Wh, fmt)
     okv = []
     if ctx_fill:
         synth.fill_kv_context(k, v, ctx_fill, seed=seed + 100)
@@ -142,6 +142,38 @@ def test_small_bf16_sd_matches_oracle(ctx_fill):
     prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
     eng, k, v, kv_len, okv, tracked, o_len, st = run_rollout(
         cfg, W, prompt, B, P + 24, gamma, T, seed, 11, tol=2e-2, ctx_fill=ctx_fill, n_steps=4)
+    say("stats", st)
+    assert st["ok"] >= 3 * B
+    assert st["exempt"] <= 2
+    eng.close()
+
+
+@pytest.mark.parametrize("fmt", ["w4a", "w8"])
+def test_tiny_fp32_sd_with_other_drafter_formats(fmt):
+    """The asymmetric-int4 and int8 drafters: every decision of a short
+    rollout of the fp32 decoder, token for token."""
+    cfg, run = synth.TINY, synth.TINY_RUN
+    say("tiny fp32 SD rollout", fmt)
+    W = synth.make_weights(cfg, run["seed"], "cpu")
+    prompt = synth.make_tokens(run["B"], run["prompt"], cfg["vocab"], run["seed"])
+    eng, k, v, kv_len, okv, tracked, o_len, st = run_rollout(
+        cfg, W, prompt, run["B"], run["prompt"] + 24, run["gamma"], run["T"], run["seed"], 3, tol=5e-3, fmt=fmt)
+    say("stats", st)
+    assert st["exempt"] == 0 and st["ok"] >= 8
+    eng.close()
+
+
+@pytest.mark.parametrize("fmt", ["w4a", "w8"])
+def test_small_bf16_sd_with_other_drafter_formats(fmt):
+    """The same for the bf16 GQA decoder over random context (the MFMA
+    drafter GEMM with split K)."""
+    cfg = SMALL_GQA
+    say("small bf16 SD", fmt)
+    B, P, gamma, T, seed = 8, 40, 4, 1.0, 6
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
+    eng, k, v, kv_len, okv, tracked, o_len, st = run_rollout(
+        cfg, W, prompt, B, P + 24, gamma, T, seed, 11, tol=2e-2, ctx_fill=300, n_steps=4, fmt=fmt)
     say("stats", st)
     assert st["ok"] >= 3 * B
     assert st["exempt"] <= 2

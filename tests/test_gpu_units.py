@@ -1,6 +1,7 @@
 """GPU parity of single SD stages through the C ABI:
-  - the drafter refresh (RTN int4 codes and fp16 scales bit-exact with the
-    oracle, unpacked from the documented tile layout);
+  - the drafter refresh in every format (RTN int4 symmetric and asymmetric,
+    int8: codes, fp16 scales and zero points bit-exact with the oracle,
+    unpacked from the documented tile layouts);
   - speculative rejection sampling on identical logits (decisions identical
     to the oracle's except at documented near-ties), for one and for many
     vocabulary chunks;
@@ -11,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from oracle.parity import drafter_layout, unpack_q4
+from oracle.parity import drafter_layout, unpack_q4, unpack_q8, unpack_zeros
 from paper_2606_18967_amd import sdrl, synth
 
 from gpu_common import host_bits, i32, make_engine, say
@@ -22,29 +23,37 @@ SMALL_BF16 = dict(name="small-bf16", n_layers=2, hidden=256, n_q=4, n_kv=2, head
                   dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
 
 
+@pytest.mark.parametrize("fmt", ["w4", "w4a", "w8"])
 @pytest.mark.parametrize("cfg", [synth.TINY, SMALL_BF16], ids=["tiny-f32", "small-bf16"])
-def test_refresh_drafter_bit_exact(cfg):
-    say("refresh_drafter", cfg["name"])
+def test_refresh_drafter_bit_exact(cfg, fmt):
+    say("refresh_drafter", cfg["name"], fmt)
     W = synth.make_weights(cfg, 5, "cpu")
-    # edge groups: all zero, huge magnitude, tiny magnitude
+    # edge groups: all zero, huge magnitude, tiny magnitude, constant
     W[4][3, 128:256] = 0
     W[4][5, :128] *= 1000
     W[8][1, 0:128] *= 1e-4
+    W[8][2, 128:256] = 0.01
     Wd = [w.cuda() for w in W]
     eng, *_ = make_engine(cfg, Wd, 1, 8, 1)
-    qbuf = eng.refresh_drafter()
+    qbuf = eng.refresh_drafter(fmt=fmt)
     torch.cuda.synchronize()
     host = qbuf.cpu().numpy()
     Wh = host_bits(W)
     kind = oracle.BF16 if cfg["dtype"] == "bf16" else oracle.F32
-    layout, total = drafter_layout(cfg)
+    layout, total = drafter_layout(cfg, fmt)
     assert total == host.size
     widx = [1, 2, 4, 5]
-    for l, w, N, K, co, so in layout:
-        codes, sc = unpack_q4(host[co:co + N * K // 2], host[so:so + N * (K // 128) * 2], N, K)
-        want_c, want_s = oracle.quantize_rtn4(oracle.tensor_f32(Wh[3 + 6 * l + widx[w]], kind))
-        assert np.array_equal(codes, want_c), (l, w)
+    for l, w, N, K, co, so, zo in layout:
+        nc = N * K // (1 if fmt == "w8" else 2)
+        if fmt == "w8":
+            codes, sc = unpack_q8(host[co:co + nc], host[so:so + N * (K // 128) * 2], N, K)
+        else:
+            codes, sc = unpack_q4(host[co:co + nc], host[so:so + N * (K // 128) * 2], N, K, fmt)
+        want_c, want_s, want_z = oracle.quantize(oracle.tensor_f32(Wh[3 + 6 * l + widx[w]], kind), fmt)
+        assert np.array_equal(codes, want_c.astype(np.int8)), (l, w)
         assert np.array_equal(sc, want_s), (l, w)
+        if fmt == "w4a":
+            assert np.array_equal(unpack_zeros(host[zo:zo + N * (K // 128)], N, K), want_z), (l, w)
     eng.close()
 
 
