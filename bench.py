@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--drafter", choices=("w4", "w4a", "w8"), default="w4",
                     help="drafter format: RTN int4 symmetric (default), int4 asymmetric, int8")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the SD steps as replays of one captured HIP graph")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -264,6 +266,17 @@ def main():
     for _ in range(n_warm):
         sd_iter()
     eng.sync()
+    eager_iter = sd_iter
+    if args.graph:
+        # the whole step as one HIP graph: fixed token buffer, kv_len advances on the device
+        last_g = tok[state["it"] % 2].clone()
+        graph = sdrl.StepGraph(eng, bufs, slots, last_g, T, seed, 1)
+
+        def sd_iter():
+            graph.replay()
+            n = bufs.n_emit.cpu()
+            state["it"] += 1
+            return int(n.sum())
 
     # ---- timed region: K SD steps
     torch.cuda.synchronize()
@@ -284,8 +297,10 @@ def main():
     eng.timing(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    if args.graph:
+        tok[state["it"] % 2].copy_(last_g)
     for _ in range(n_steps):
-        sd_iter()
+        eager_iter()
     torch.cuda.synchronize()
     dt_prof = time.perf_counter() - t0
     classes = {}
@@ -359,7 +374,7 @@ def main():
         "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + "
                                + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
                                + " drafter, B=64, KV context 2048 (random N(0,1)), gamma=4, T=1.0",
-                   "drafter": args.drafter,
+                   "drafter": args.drafter, "hip_graph": bool(args.graph),
                    "batch": B, "context": S, "gamma": gamma, "temperature": T, "layers": L, "hidden": H,
                    "heads": f"{nq}q/{nkv}kv x {d}", "ffn": F, "vocab": V},
         "roofline": roof,

@@ -325,6 +325,30 @@ def sd_step(eng: Engine, bufs: SDBuffers, slots, last_tok, T, seed, step):
     eng.rollback(slots, bufs.n_emit)
 
 
+class StepGraph:
+    """One SD step for a fixed batch (slots, last_tok, buffers, gamma, T and
+    the Philox key), captured once as a HIP graph through torch: draft,
+    verify, accept, rollback, then last_tok <- next_tok.  Every launch of the
+    step takes its positions from kv_len on the device, so each replay
+    advances the sequences exactly as the eager calls would.  Call after at
+    least one eager step (kernels loaded); timing must be off while capturing.
+    replay() enqueues the step on the current stream; the host still reads
+    n_emit from bufs after it."""
+
+    def __init__(self, eng: Engine, bufs: SDBuffers, slots, last_tok, T, seed, step):
+        self.eng, self.bufs, self.slots, self.last_tok = eng, bufs, slots, last_tok
+        self.graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(device=eng.device)            # default priority
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(self.graph, stream=side):
+            sd_step(eng, bufs, slots, last_tok, T, seed, step)
+            torch.add(bufs.next_tok, 0, out=last_tok)             # a kernel node, not a copy node
+        torch.cuda.current_stream().wait_stream(side)
+
+    def replay(self):
+        self.graph.replay()
+
+
 def dense_gemm_bf16(A: torch.Tensor, W: torch.Tensor, out: torch.Tensor):
     """out[M][N] (fp32) = A[M][K] W[N][K]^T with the library's bf16 GEMM kernels."""
     M, K = A.shape
