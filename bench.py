@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--drafter", choices=("w4", "w4a", "w8"), default="w4",
                     help="drafter format: RTN int4 symmetric (default), int4 asymmetric, int8")
+    ap.add_argument("--page-size", type=int, default=0,
+                    help="bind a paged KV cache with pages of this many positions, shuffled (0: dense cache)")
     ap.add_argument("--graph", action="store_true",
                     help="time the SD steps as replays of one captured HIP graph")
     ap.add_argument("--quiet", action="store_true")
@@ -229,9 +231,24 @@ def main():
     W = synth.make_weights(cfg, seed, dev)
     eng = sdrl.Engine(cfg, B, max_ctx, gamma)
     eng.bind_weights(W)
-    k, v, kv_len = eng.alloc_kv()
-    eng.bind_kv(k, v, kv_len)
-    synth.fill_kv_context(k, v, S, seed + 100)
+    if args.page_size:
+        # paged cache: every sequence's pages drawn at random from one pool
+        P = args.page_size
+        pps = (max_ctx + P - 1) // P
+        perm = torch.randperm(B * pps, generator=torch.Generator().manual_seed(seed + 3))
+        table = perm.to(torch.int32).reshape(B, pps).to(dev).contiguous()
+        k, v, kv_len = eng.alloc_kv_paged(B * pps, P)
+        eng.bind_kv_paged(k, v, table, kv_len)
+        L_, Hk, D_ = cfg["n_layers"], cfg["n_kv"], cfg["head_dim"]
+        g = torch.Generator(device=dev).manual_seed(seed + 100)
+        for j in range((S + P - 1) // P):           # random N(0, 1) context in the first S positions
+            n = min(P, S - j * P)
+            for t in (k, v):
+                t[table[:, j].long(), :, :, :n] = torch.randn((B, L_, Hk, n, D_), generator=g, device=dev).to(t.dtype)
+    else:
+        k, v, kv_len = eng.alloc_kv()
+        eng.bind_kv(k, v, kv_len)
+        synth.fill_kv_context(k, v, S, seed + 100)
     kv_len.fill_(S)
     torch.cuda.synchronize()
     # drafter refresh (the per-training-step Prep): once to load the kernels,
@@ -355,7 +372,7 @@ def main():
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.page_size:
         cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, args.drafter)
 
     rec = {
@@ -374,7 +391,7 @@ def main():
         "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + "
                                + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
                                + " drafter, B=64, KV context 2048 (random N(0,1)), gamma=4, T=1.0",
-                   "drafter": args.drafter, "hip_graph": bool(args.graph),
+                   "drafter": args.drafter, "hip_graph": bool(args.graph), "kv_page_size": args.page_size,
                    "batch": B, "context": S, "gamma": gamma, "temperature": T, "layers": L, "hidden": H,
                    "heads": f"{nq}q/{nkv}kv x {d}", "ffn": F, "vocab": V},
         "roofline": roof,

@@ -110,6 +110,27 @@ size_t sd_kv_bytes(const sd_model_cfg* cfg, int32_t max_slots, int32_t max_ctx);
  * (device int32[max_slots]).  K holds post-RoPE keys. */
 sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len);
 
+/* Bytes of EACH of the K and V pages of a paged cache: n_layers*n_kv*
+ * page_size*head_dim elements of the model dtype (0 for page_size < 1). */
+size_t sd_kv_page_bytes(const sd_model_cfg* cfg, int32_t page_size);
+
+/* Binds a paged KV cache instead (the page-granular memory of serving
+ * engines the paper's rollouts run in, Sec. 4.1 and App. B.2): K and V pools
+ * of n_pages pages, each laid out [L][n_kv][page_size][head_dim], and a
+ * block table block_table (device int32 [max_slots][pages_per_seq]) whose
+ * entry (slot, j) names the page holding that slot's positions
+ * [j*page_size, (j+1)*page_size).  All three are caller-owned and read by
+ * every later call; the caller may change table entries between calls (e.g.
+ * hand pages of finished sequences to new ones) but not while a call it
+ * enqueued is running.  Positions are still kv_len-relative: rollback only
+ * moves kv_len, and pages past it stay the caller's to reuse.  Requires
+ * page_size a multiple of 32 and pages_per_seq*page_size >= max_ctx
+ * (SD_E_INVAL otherwise).  A table entry outside [0, n_pages) met on the
+ * device is skipped and reported by sd_sync as SD_E_INVAL.  Replaces any
+ * earlier binding. */
+sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages, int32_t n_pages, int32_t page_size,
+                           const int32_t* block_table, int32_t pages_per_seq, int32_t* kv_len);
+
 /* Drafter weight formats (RTN, groups of 128 weights along K, one fp16 scale
  * per (output column, group)): int4 symmetric (Sec. 4.1, the default), int4
  * asymmetric with a zero point per (column, group) (App. B.2), and int8

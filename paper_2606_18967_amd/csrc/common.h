@@ -86,6 +86,7 @@ enum : int {
     ERR_SLOT = 0,       // slot index outside [0, max_slots)
     ERR_TOKEN = 1,      // token id outside [0, vocab)
     ERR_CTX = 2,        // a position at or beyond max_ctx
+    ERR_PAGE = 3,       // a block-table entry outside [0, n_pages) (paged KV)
     ERR_COUNT = 4
 };
 __device__ __forceinline__ void flag_error(uint32_t* err, int kind) { ((volatile uint32_t*)err)[kind] = 1u; }

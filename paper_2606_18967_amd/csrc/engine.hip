@@ -59,6 +59,7 @@ struct sd_engine_s {
     void* k = nullptr;
     void* v = nullptr;
     int32_t* kv_len = nullptr;
+    kv_geom geo = {};                  // dense or paged layout of k / v
     std::vector<const uint32_t*> qw;   // [L*4] packed codes
     std::vector<const uint16_t*> qs;   // [L*4] scales
     std::vector<const uint8_t*> qz;    // [L*4] zero points (asymmetric format), else NULL
@@ -313,6 +314,33 @@ extern "C" sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len)
     e->k = k;
     e->v = v;
     e->kv_len = kv_len;
+    const long long D = e->c.head_dim, H = e->c.n_kv, C = e->max_ctx;
+    e->geo = kv_geom{e->max_ctx, H * C * D, (long long)e->max_slots * H * C * D, C * D, nullptr, 1, e->max_slots};
+    return SD_OK;
+}
+
+extern "C" size_t sd_kv_page_bytes(const sd_model_cfg* c, int32_t page_size)
+{
+    if (!c || page_size < 1) return 0;
+    size_t el = c->dtype == SD_DTYPE_F32 ? 4 : 2;
+    return (size_t)c->n_layers * c->n_kv * (size_t)page_size * c->head_dim * el;
+}
+
+extern "C" sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages, int32_t n_pages, int32_t page_size,
+                                      const int32_t* block_table, int32_t pages_per_seq, int32_t* kv_len)
+{
+    if (!e || !k_pages || !v_pages || !block_table || !kv_len) return fail(SD_E_INVAL, "NULL argument");
+    if (n_pages < 1 || page_size < 32 || page_size % 32)
+        return fail(SD_E_INVAL, "need n_pages >= 1 and page_size a positive multiple of 32 (got %d, %d)", n_pages,
+                    page_size);
+    if (pages_per_seq < 1 || (long long)pages_per_seq * page_size < e->max_ctx)
+        return fail(SD_E_INVAL, "pages_per_seq * page_size = %lld must cover max_ctx = %d",
+                    (long long)pages_per_seq * page_size, e->max_ctx);
+    e->k = k_pages;
+    e->v = v_pages;
+    e->kv_len = kv_len;
+    const long long D = e->c.head_dim, H = e->c.n_kv, L = e->c.n_layers, P = page_size;
+    e->geo = kv_geom{page_size, L * H * P * D, H * P * D, P * D, block_table, pages_per_seq, n_pages};
     return SD_OK;
 }
 
@@ -400,7 +428,7 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
 {
     const sd_model_cfg& c = e->c;
     rows_t r = {B, n, off, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
-    cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, c.n_kv, c.head_dim};
+    cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, c.n_kv, c.head_dim, e->geo};
     const int R = B * n;
     const act_t at = act_of(e, draft);
     const int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
@@ -532,7 +560,7 @@ extern "C" sd_status kv_rollback(sd_engine e, int32_t B, const int32_t* slots, c
     tscope t(e, T_MISC, s);
     launch_kv_advance(B, slots, n_emit, 0, e->kv_len, e->max_slots, e->err, s);
     if (e->poison) {
-        cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, e->c.n_kv, e->c.head_dim};
+        cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, e->c.n_kv, e->c.head_dim, e->geo};
         launch_kv_poison(B, slots, e->kv_len, e->max_gamma + 1, kv, e->c.n_layers, e->max_slots, e->max_ctx, s);
     }
     return launched("kv_rollback");
@@ -564,6 +592,7 @@ extern "C" sd_status sd_sync(sd_engine e, void* stream)
     if (flags[ERR_SLOT]) return fail(SD_E_INVAL, "device: slot index outside [0, max_slots)");
     if (flags[ERR_TOKEN]) return fail(SD_E_INVAL, "device: token id outside [0, vocab)");
     if (flags[ERR_CTX]) return fail(SD_E_INVAL, "device: position at or beyond max_ctx");
+    if (flags[ERR_PAGE]) return fail(SD_E_INVAL, "device: block-table entry outside [0, n_pages)");
     if (e->launch_err) { e->launch_err = 0; return fail(SD_E_UNSUPPORTED, "an int4 GEMM shape was refused"); }
     return SD_OK;
 }

@@ -18,12 +18,26 @@ struct rows_t {
     uint32_t* err;          // device error words
 };
 
-// Cache geometry: k/v are [L][max_slots][n_kv][max_ctx][head_dim].
+// KV cache geometry.  The element offset of (slot, layer, KV head h,
+// position p) is page * PS + layer * LS + h * HS + (p % P) * head_dim, with
+//   dense cache [L][max_slots][n_kv][max_ctx][head_dim]: P = max_ctx and
+//     page = slot;
+//   paged cache, pages [n_pages][L][n_kv][P][head_dim]: page =
+//     bt[slot * mpp + p / P] from the caller's block table (an entry outside
+//     [0, n_pages) is reported as ERR_PAGE and its positions are skipped).
+struct kv_geom {
+    int P;                     // positions per page
+    long long PS, LS, HS;      // element strides of a page, a layer and a KV head
+    const int32_t* bt;         // device int32 [max_slots][mpp], or NULL for the dense cache
+    int mpp, n_pages;
+};
+
 struct cache_t {
     void* k;
     void* v;
     int kv_f32;             // 1: fp32 cache, 0: bf16 cache
     int n_kv, head_dim;
+    kv_geom g;
 };
 
 // ---- model kernels (kernels_model.hip)

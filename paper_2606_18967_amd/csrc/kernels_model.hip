@@ -8,6 +8,17 @@
 
 namespace {
 
+// physical page holding logical page lp of a slot's positions, or -1 when the
+// block table has no valid page there (kv_geom, kernels.h)
+__device__ __forceinline__ long long kv_page(const kv_geom& g, int slot, int lp)
+{
+    if (!g.bt) return slot;
+    if (lp < 0 || lp >= g.mpp) return -1;
+    const int pg = g.bt[(size_t)slot * g.mpp + lp];
+    return pg >= 0 && pg < g.n_pages ? pg : -1;
+}
+
+
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef short v8s __attribute__((ext_vector_type(8)));
 
@@ -133,8 +144,8 @@ __device__ __forceinline__ float sum_parts(const float* src, const float* P, int
 // k + d/2 of the unit.
 template <typename T>
 __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, const float* P, int S, const float2* rope,
-                                                 int n_q, int n_kv, int d, T* kc, T* vc, int layer, float* q_out,
-                                                 int upw)
+                                                 int n_q, int n_kv, int d, T* kc, T* vc, kv_geom g, int layer,
+                                                 float* q_out, int upw)
 {
     const int row = blockIdx.x;
     int b, i, slot, pos;
@@ -156,7 +167,10 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
         return;
     }
     const float2* rp = rope + (size_t)pos * hd;
-    const size_t cbase = (((size_t)layer * r.max_slots + slot) * n_kv) * (size_t)r.max_ctx;
+    // this row's K/V position: page, then layer and offset in the page
+    const long long pg = kv_page(g, slot, pos / g.P);
+    if (pg < 0 && threadIdx.x == 0 && blockIdx.y == 0) flag_error(r.err, ERR_PAGE);
+    const long long cbase = pg * g.PS + layer * g.LS + (long long)(pos % g.P) * d;
     for (int t = threadIdx.x; t < nu * hd; t += blockDim.x) {
         const int u = u0 + t / hd, k = t - (t / hd) * hd;
         const size_t c0 = base_idx + (size_t)u * d + k;
@@ -167,13 +181,13 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
             if (u < n_q) {
                 qo[(size_t)u * d + k] = x0;
                 qo[(size_t)u * d + k + hd] = x1;
-            } else {
-                const size_t o = (cbase + (size_t)(u - n_q) * r.max_ctx + pos) * d;
+            } else if (pg >= 0) {
+                const size_t o = cbase + (u - n_q) * g.HS;
                 elem<T>::store(kc, o + k, x0);
                 elem<T>::store(kc, o + k + hd, x1);
             }
-        } else {
-            const size_t o = (cbase + (size_t)(u - n_q - n_kv) * r.max_ctx + pos) * d;
+        } else if (pg >= 0) {
+            const size_t o = cbase + (u - n_q - n_kv) * g.HS;
             elem<T>::store(vc, o + k, a);
             elem<T>::store(vc, o + k + hd, c);
         }
@@ -192,7 +206,7 @@ constexpr int ATT_RG = 4;   // query rows per pass
 
 template <typename T, int D>
 __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, int n_q, int n_kv,
-                                                      const T* kc, const T* vc, int layer, float* part,
+                                                      const T* kc, const T* vc, kv_geom kg, int layer, float* part,
                                                       int max_chunks)
 {
     constexpr int LPP = D / 8;          // lanes per position
@@ -219,9 +233,7 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
     int G = n_q / n_kv;
     int QR = G * r.n;
     float scale = rsqrtf((float)D);
-    size_t cbase = ((((size_t)layer * r.max_slots + slot) * n_kv + kvh) * (size_t)r.max_ctx) * D;
-    const T* K = kc + cbase;
-    const T* Vv = vc + cbase;
+    const long long hbase = layer * kg.LS + kvh * kg.HS;      // + page * PS + (p % P) * D
 
     for (int rg0 = 0; rg0 < QR; rg0 += ATT_RG) {
         float qv[ATT_RG][8], m[ATT_RG], l[ATT_RG], o[ATT_RG][8];
@@ -242,9 +254,15 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
             int p = pb + pg;
             bool pv = p < p1;
             float kf[8], vf[8];
+            long long page = pv ? kv_page(kg, slot, p / kg.P) : 0;
+            if (page < 0) {
+                if ((lane % LPP) == 0) flag_error(r.err, ERR_PAGE);
+                pv = false;
+            }
             if (pv) {
+                const size_t o = page * kg.PS + hbase + (long long)(p % kg.P) * D + dd;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) { kf[e] = elem<T>::load(K, (size_t)p * D + dd + e); vf[e] = elem<T>::load(Vv, (size_t)p * D + dd + e); }
+                for (int e = 0; e < 8; ++e) { kf[e] = elem<T>::load(kc, o + e); vf[e] = elem<T>::load(vc, o + e); }
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) { kf[e] = 0.f; vf[e] = 0.f; }
@@ -333,9 +351,9 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 
 // two waves per SIMD where the registers allow it without spills (one query
 // tile); the verify variants keep one
-template <int D, int MQ>
+template <int D, int MQ, bool PAGED>
 __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
-                                                   const uint16_t* vc, int layer, float* part, int max_chunks, int ch)
+                                                   const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch)
 {
     constexpr int KS = D / 32;      // k-steps over the head dim
     constexpr int NBD = D / 16;     // 16-wide blocks of the head dim
@@ -371,9 +389,9 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     bf16x8 qf[MQ][KS];
     int lim[MQ];
 
-    const size_t cbase = ((((size_t)layer * r.max_slots + slot) * n_kv + kvh) * (size_t)r.max_ctx) * D;
-    const uint16_t* K = kc + cbase;
-    const uint16_t* V = vc + cbase;
+    const long long hbase = layer * kg.LS + kvh * kg.HS;      // + page * PS (+ (p % P) * D)
+    const uint16_t* K = kc + (PAGED ? 0 : slot * kg.PS) + hbase;
+    const uint16_t* V = vc + (PAGED ? 0 : slot * kg.PS) + hbase;
     uint16_t* vs = Vs[w];
 
     float m[MQ], lsum[MQ];
@@ -391,13 +409,26 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     // K fragments of the two 16-position tiles and the V block of the block at
     // blk, through buffer resources limited to the cached positions: reads at
     // or past ctx return 0 without touching memory.  Positions past the wave's
-    // range get -inf scores below, so their P is 0.
-    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, ctx * D * 2, 0x00020000);
-    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)V, 0, ctx * D * 2, 0x00020000);
+    // range get -inf scores below, so their P is 0.  The dense cache has one
+    // resource per sequence; the paged one a resource per page (a block of 32
+    // positions never straddles pages), none (0 records) for a missing page.
+    __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, ctx * D * 2, 0x00020000);
+    __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)V, 0, ctx * D * 2, 0x00020000);
     const int koff = (lr * D + 8 * cq) * 2;                         // + (16 pt) D 2 + 64 ks
     const int voff = ((lane / CPP) * D + (lane % CPP) * 8) * 2;     // + t (64 / CPP) D 2
     auto load_kv = [&](int blk, u32x4 (&kf)[2][KS], u32x4 (&vv)[CPP / 2]) {
-        const int sb = __builtin_amdgcn_readfirstlane(blk * D * 2);   // scalar offset of the block
+        int sb = __builtin_amdgcn_readfirstlane(blk * D * 2);         // scalar offset of the block
+        if constexpr (PAGED) {
+            const int lp = __builtin_amdgcn_readfirstlane(blk / kg.P), in0 = lp * kg.P;
+            long long pg = kv_page(kg, slot, lp);
+            pg = __builtin_amdgcn_readfirstlane((int)pg);
+            if (pg < 0 && lane == 0 && blk < ctx) flag_error(r.err, ERR_PAGE);
+            const int nrec = pg < 0 ? 0 : max(0, min(kg.P, ctx - in0)) * D * 2;
+            const long long po = (pg < 0 ? 0 : pg) * kg.PS;
+            krs = __builtin_amdgcn_make_buffer_rsrc((void*)(K + po), 0, nrec, 0x00020000);
+            vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(V + po), 0, nrec, 0x00020000);
+            sb = __builtin_amdgcn_readfirstlane((blk - in0) * D * 2);
+        }
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
@@ -634,7 +665,7 @@ __global__ void k_kv_advance(int B, const int32_t* slots, const int32_t* inc, in
 }
 
 template <typename T>
-__global__ void k_kv_poison(const int32_t* slots, const int32_t* kv_len, int span, T* kc, T* vc,
+__global__ void k_kv_poison(const int32_t* slots, const int32_t* kv_len, int span, T* kc, T* vc, kv_geom g,
                             int n_layers, int n_kv, int D, int max_slots, int max_ctx)
 {
     int b = blockIdx.x;
@@ -649,7 +680,10 @@ __global__ void k_kv_poison(const int32_t* slots, const int32_t* kv_len, int spa
         size_t lh = t / per;
         int rem = (int)(t - lh * per);
         int l = (int)(lh / n_kv), h = (int)(lh - (size_t)l * n_kv);
-        size_t o = ((((size_t)l * max_slots + s) * n_kv + h) * max_ctx + p0) * D + rem;
+        const int p = p0 + rem / D;
+        const long long pg = kv_page(g, s, p / g.P);
+        if (pg < 0) continue;
+        size_t o = pg * g.PS + l * g.LS + h * g.HS + (long long)(p % g.P) * D + rem % D;
         elem<T>::store(kc, o, __int_as_float(0x7fc00000));
         elem<T>::store(vc, o, __int_as_float(0x7fc00000));
     }
@@ -702,10 +736,10 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, co
     dim3 grid(R, (units + upw - 1) / upw);
     if (c.kv_f32)
         k_rope_kv<float><<<grid, 256, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (float*)c.k, (float*)c.v,
-                                              layer, q_out, upw);
+                                              c.g, layer, q_out, upw);
     else
         k_rope_kv<uint16_t><<<grid, 256, 0, s>>>(r, qkv, P, S, rope, n_q, c.n_kv, c.head_dim, (uint16_t*)c.k,
-                                                 (uint16_t*)c.v, layer, q_out, upw);
+                                                 (uint16_t*)c.v, c.g, layer, q_out, upw);
 }
 
 int attention_chunk() { return ATT_CH < ATT_MIN_CHUNK ? ATT_CH : ATT_MIN_CHUNK; }
@@ -713,6 +747,20 @@ int attention_chunk() { return ATT_CH < ATT_MIN_CHUNK ? ATT_CH : ATT_MIN_CHUNK; 
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
 {
     return (size_t)R * n_q * max_chunks * (head_dim + 2);
+}
+
+template <int D, bool PAGED>
+static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, const rows_t& r, const float* q, int n_q,
+                             const cache_t& c, int layer, float* part, int mch, int ch)
+{
+    const uint16_t* kc = (const uint16_t*)c.k;
+    const uint16_t* vc = (const uint16_t*)c.v;
+    switch (MQ) {
+        case 1: k_attn_mfma<D, 1, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
+        case 2: k_attn_mfma<D, 2, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
+        case 3: k_attn_mfma<D, 3, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
+        default: k_attn_mfma<D, 4, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
+    }
 }
 
 template <typename T, int D>
@@ -735,18 +783,13 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
             ch = ((r.max_ctx + mch - 1) / mch + 31) & ~31;
         }
         dim3 grid(r.B * c.n_kv, mch, zs);
-        const uint16_t* kc = (const uint16_t*)c.k;
-        const uint16_t* vc = (const uint16_t*)c.v;
-        switch (MQ) {
-            case 1: k_attn_mfma<D, 1><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
-            case 2: k_attn_mfma<D, 2><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
-            case 3: k_attn_mfma<D, 3><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
-            default: k_attn_mfma<D, 4><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, layer, part, mch, ch); break;
-        }
+        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch);
+        else attn_mfma_launch<D, false>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch);
         return attn_split{mch, ch};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
-        k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, layer, part, max_chunks);
+        k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, c.g, layer, part,
+                                                  max_chunks);
         return attn_split{max_chunks, ATT_CH};
     }
 }
@@ -789,9 +832,9 @@ void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int sp
                       int n_layers, int max_slots, int max_ctx, hipStream_t s)
 {
     if (c.kv_f32)
-        k_kv_poison<float><<<B, 256, 0, s>>>(slots, kv_len, span, (float*)c.k, (float*)c.v, n_layers, c.n_kv,
+        k_kv_poison<float><<<B, 256, 0, s>>>(slots, kv_len, span, (float*)c.k, (float*)c.v, c.g, n_layers, c.n_kv,
                                              c.head_dim, max_slots, max_ctx);
     else
-        k_kv_poison<uint16_t><<<B, 256, 0, s>>>(slots, kv_len, span, (uint16_t*)c.k, (uint16_t*)c.v, n_layers,
+        k_kv_poison<uint16_t><<<B, 256, 0, s>>>(slots, kv_len, span, (uint16_t*)c.k, (uint16_t*)c.v, c.g, n_layers,
                                                 c.n_kv, c.head_dim, max_slots, max_ctx);
 }

@@ -27,7 +27,7 @@ SD_DTYPE_F32, SD_DTYPE_BF16 = 0, 1
 # The names every build must export (one per declaration in include/sd_api.h).
 API_SYMBOLS = (
     "sd_last_error", "sd_create", "sd_destroy", "sd_num_weights", "sd_bind_weights", "sd_kv_bytes",
-    "sd_bind_kv", "sd_drafter_bytes", "sd_drafter_bytes_fmt", "sd_refresh_drafter", "sd_refresh_drafter_fmt",
+    "sd_bind_kv", "sd_kv_page_bytes", "sd_bind_kv_paged", "sd_drafter_bytes", "sd_drafter_bytes_fmt", "sd_refresh_drafter", "sd_refresh_drafter_fmt",
     "sd_prefill", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
@@ -91,6 +91,8 @@ def lib():
             "sd_bind_kv": (_i32, [_P, _P, _P, _P]),
             "sd_drafter_bytes": (_sz, [_P]),
             "sd_refresh_drafter": (_i32, [_P, _P, _sz, _P]),
+            "sd_kv_page_bytes": (_sz, [_P, _i32]),
+            "sd_bind_kv_paged": (_i32, [_P, _P, _P, _i32, _i32, _P, _i32, _P]),
             "sd_drafter_bytes_fmt": (_sz, [_P, _i32]),
             "sd_refresh_drafter_fmt": (_i32, [_P, _i32, _P, _sz, _P]),
             "sd_prefill": (_i32, [_P, _i32, _P, _P, _i32, _P]),
@@ -212,6 +214,28 @@ class Engine:
                                 _dev(v, "v", self.wdtype, shp, self.device),
                                 _dev(kv_len, "kv_len", torch.int32, (self.max_slots,), self.device)))
         self._keep_kv = (k, v, kv_len)
+
+    def alloc_kv_paged(self, n_pages: int, page_size: int):
+        """K and V page pools [n_pages][L][n_kv][page_size][head_dim] and kv_len."""
+        c = self.cfg
+        shp = (n_pages, c["n_layers"], c["n_kv"], page_size, c["head_dim"])
+        k = torch.zeros(shp, dtype=self.wdtype, device=self.device)
+        v = torch.zeros(shp, dtype=self.wdtype, device=self.device)
+        kv_len = torch.zeros(self.max_slots, dtype=torch.int32, device=self.device)
+        return k, v, kv_len
+
+    def bind_kv_paged(self, k, v, block_table, kv_len):
+        """Paged cache: pools from alloc_kv_paged and an int32 block table
+        [max_slots][pages_per_seq] of page indices (both caller-owned)."""
+        n_pages, page_size = k.shape[0], k.shape[3]
+        c = self.cfg
+        shp = (n_pages, c["n_layers"], c["n_kv"], page_size, c["head_dim"])
+        pps = block_table.shape[1]
+        _check(lib().sd_bind_kv_paged(self.h, _dev(k, "k", self.wdtype, shp, self.device),
+                                      _dev(v, "v", self.wdtype, shp, self.device), n_pages, page_size,
+                                      _dev(block_table, "block_table", torch.int32, (self.max_slots, pps), self.device),
+                                      pps, _dev(kv_len, "kv_len", torch.int32, (self.max_slots,), self.device)))
+        self._keep_kv = (k, v, block_table, kv_len)
 
     def drafter_bytes(self, fmt: str = "w4") -> int:
         return int(lib().sd_drafter_bytes_fmt(C.byref(self.c), DRAFT_FORMATS[fmt]))

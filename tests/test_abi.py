@@ -89,3 +89,6 @@ def test_sizes():
     assert L.sd_drafter_bytes_fmt(C.byref(c), -1) == 0
     # host-side argument checks of the refresh need no device
     assert L.sd_refresh_drafter_fmt(None, 1, None, 0, None) == 1      # SD_E_INVAL
+    assert L.sd_kv_page_bytes(C.byref(c), 64) == 4 * 8 * 64 * 128 * 2
+    assert L.sd_kv_page_bytes(C.byref(c), 0) == 0
+    assert L.sd_bind_kv_paged(None, None, None, 4, 64, None, 4, None) == 1
