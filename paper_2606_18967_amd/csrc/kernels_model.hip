@@ -342,6 +342,9 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 // sequence for about ATT_TARGET_WGS work-groups in all (two per CU), each at
 // least ATT_MIN_CHUNK positions, so a large batch streams a whole context per
 // work-group and a small one still fills the GPU.
+#ifndef ATT_INTERLEAVE
+#define ATT_INTERLEAVE 1
+#endif
 #ifndef ATT_TARGET_WGS
 #define ATT_TARGET_WGS 512
 #endif
@@ -404,8 +407,14 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
         for (int nb = 0; nb < NBD; ++nb) o[mt][nb] = (floatx4){0.f, 0.f, 0.f, 0.f};
     }
 
+#if ATT_INTERLEAVE
+    // the four waves take the chunk's 32-position blocks in turn, so the
+    // work-group reads K and V as two contiguous streams
+    const int wq0 = p0 + 32 * w, wq1 = p1, wstep = 128;
+#else
     const int wlen = ((clen + 3) / 4 + 31) & ~31;                  // positions per wave
-    const int wq0 = p0 + w * wlen, wq1 = min(wq0 + wlen, p1);
+    const int wq0 = p0 + w * wlen, wq1 = min(wq0 + wlen, p1), wstep = 32;
+#endif
     // K fragments of the two 16-position tiles and the V block of the block at
     // blk, through buffer resources limited to the cached positions: reads at
     // or past ctx return 0 without touching memory.  Positions past the wave's
@@ -551,12 +560,12 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
         }
     }
 
-    for (int blk = wq0; blk < wq1; blk += 64) {
-        load_kv(blk + 32, kf1, vv1);
+    for (int blk = wq0; blk < wq1; blk += 2 * wstep) {
+        load_kv(blk + wstep, kf1, vv1);
         block(blk, kf0, vv0);
-        if (blk + 32 >= wq1) break;
-        load_kv(blk + 64, kf0, vv0);
-        block(blk + 32, kf1, vv1);
+        if (blk + wstep >= wq1) break;
+        load_kv(blk + 2 * wstep, kf0, vv0);
+        block(blk + wstep, kf1, vv1);
     }
 #pragma unroll
     for (int mt = 0; mt < MQ; ++mt) {
