@@ -53,9 +53,11 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, co
                     const cache_t& c, int layer, float* q_out, hipStream_t s);
 // Attention in two launches: per-chunk partial softmax-weighted sums into
 // part, then the combine over chunks into out.
-struct attn_split { int chunks, chunk; };
+// chunks and chunk length of a split-context attention launch; done when
+// each sequence was a single chunk and the kernel wrote the output itself
+struct attn_split { int chunks, chunk; bool done; };
 attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, hipStream_t s);
+                            int max_chunks, void* out, act_t out_t, hipStream_t s);
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
                               act_t out_t, hipStream_t s);
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks);

@@ -356,7 +356,8 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 // tile); the verify variants keep one
 template <int D, int MQ, bool PAGED>
 __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
-                                                   const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch)
+                                                   const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch,
+                                                   void* out, int out_t)
 {
     constexpr int KS = D / 32;      // k-steps over the head dim
     constexpr int NBD = D / 16;     // 16-wide blocks of the head dim
@@ -370,7 +371,19 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
     // wave-uniform by construction; readfirstlane lets the compiler keep them
     // (and the buffer resources built from them) in scalar registers
     const int slot = __builtin_amdgcn_readfirstlane(r.slots[b]);
-    if (slot < 0 || slot >= r.max_slots) return;   // flagged by k_rope_kv
+    if (slot < 0 || slot >= r.max_slots) {         // flagged by k_rope_kv; a direct output is zeroed
+        const int G = n_q / n_kv;
+        for (int idx = threadIdx.x; out && idx < 16 * MQ * D; idx += 256) {
+            const int qrow = z * 16 * MQ + idx / D, d = idx % D;
+            if (qrow >= G * r.n) continue;
+            const int g = qrow / r.n, i = qrow - g * r.n;
+            const size_t oi = ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D + d;
+            if (out_t == ACT_F16) store_act<_Float16>(out, oi, 0.f);
+            else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, 0.f);
+            else store_act<float>(out, oi, 0.f);
+        }
+        return;
+    }
     const int basepos = __builtin_amdgcn_readfirstlane(r.kv_len[slot]) + r.off;
     int ctx = basepos + r.n;
     if (ctx > r.max_ctx) ctx = r.max_ctx;
@@ -602,6 +615,16 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
                 }
             }
             const int g = qrow / r.n, i = qrow - g * r.n;
+            if (out) {
+                // a single chunk per sequence: the normalized output directly (what
+                // k_attn_combine computes from one chunk)
+                const size_t oi = ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D + d;
+                const float v = ls > 0.f ? os / ls : 0.f;
+                if (out_t == ACT_F16) store_act<_Float16>(out, oi, v);
+                else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, v);
+                else store_act<float>(out, oi, v);
+                continue;
+            }
             float* pp = part + (((size_t)(b * r.n + i) * n_q + kvh * G + g) * max_chunks + c) * (D + 2);
             if (d == 0) { pp[0] = mm * LN2; pp[1] = ls; }
             pp[2 + d] = os;
@@ -760,21 +783,21 @@ size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
 
 template <int D, bool PAGED>
 static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, const rows_t& r, const float* q, int n_q,
-                             const cache_t& c, int layer, float* part, int mch, int ch)
+                             const cache_t& c, int layer, float* part, int mch, int ch, void* out, int out_t)
 {
     const uint16_t* kc = (const uint16_t*)c.k;
     const uint16_t* vc = (const uint16_t*)c.v;
     switch (MQ) {
-        case 1: k_attn_mfma<D, 1, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
-        case 2: k_attn_mfma<D, 2, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
-        case 3: k_attn_mfma<D, 3, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
-        default: k_attn_mfma<D, 4, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch); break;
+        case 1: k_attn_mfma<D, 1, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
+        case 2: k_attn_mfma<D, 2, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
+        case 3: k_attn_mfma<D, 3, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
+        default: k_attn_mfma<D, 4, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
     }
 }
 
 template <typename T, int D>
 static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                         int max_chunks, hipStream_t s)
+                         int max_chunks, void* out, act_t out_t, hipStream_t s)
 {
     if constexpr (sizeof(T) == 2) {
         // bf16 cache: MFMA kernel.  max_chunks (the partial buffer's chunk
@@ -792,26 +815,28 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
             ch = ((r.max_ctx + mch - 1) / mch + 31) & ~31;
         }
         dim3 grid(r.B * c.n_kv, mch, zs);
-        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch);
-        else attn_mfma_launch<D, false>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch);
-        return attn_split{mch, ch};
+        // one chunk per sequence: the kernel writes the final output itself
+        void* o = mch == 1 ? out : nullptr;
+        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch, o, out_t);
+        else attn_mfma_launch<D, false>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch, o, out_t);
+        return attn_split{mch, ch, o != nullptr};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
         k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, c.g, layer, part,
                                                   max_chunks);
-        return attn_split{max_chunks, ATT_CH};
+        return attn_split{max_chunks, ATT_CH, false};
     }
 }
 
 attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, hipStream_t s)
+                            int max_chunks, void* out, act_t out_t, hipStream_t s)
 {
     if (c.head_dim == 128) {
-        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, s);
-        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, s);
+        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
     }
-    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, s);
-    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, s);
+    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
 }
 
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,

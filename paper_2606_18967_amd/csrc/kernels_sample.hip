@@ -162,65 +162,98 @@ __global__ void __launch_bounds__(STHREADS) k_stats_partial(const float* logits,
     if (threadIdx.x == 0) { part[((size_t)row * nch + ch) * 2] = v.m; part[((size_t)row * nch + ch) * 2 + 1] = v.s; }
 }
 
-__device__ float lse_of(const float* part, int row, int nch)
-{
-    const float* p = part + (size_t)row * nch * 2;
-    float m = -INFINITY;
-    for (int c = 0; c < nch; ++c) m = fmaxf(m, p[2 * c]);
-    float s = 0.f;
-    for (int c = 0; c < nch; ++c) if (p[2 * c + 1] > 0.f) s += p[2 * c + 1] * __expf(p[2 * c] - m);
-    return m + logf(s);
-}
-
 // work[b] = {mode (0 residual, 1 bonus), p row, lse_p, lse_q, position, n_emit}
 constexpr int WK = 6;
 
-__global__ void k_accept_decide(rows_t r, int gamma, int V, float invT, rng_t rng, const int32_t* draft,
-                                const float* q_logits, const float* q_stats, const float* p_logits,
-                                const float* spart, int nch, int32_t* out_tok, int32_t* n_emit, float* work)
+// log-sum-exp of p row `row` from its chunk partials, reduced over one wave
+// (lane c takes chunks c, c + 64, ...; the same butterfly order every time)
+__device__ float wave_lse(const float* part, int row, int nch, int lane)
 {
-    int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= r.B) return;
-    int slot = r.slots[b];
+    const float* p = part + (size_t)row * nch * 2;
+    float m = -INFINITY, s = 0.f;
+    for (int c = lane; c < nch; c += 64) {
+        const float mc = p[2 * c], sc = p[2 * c + 1];
+        if (!(sc > 0.f)) continue;
+        const float mn = fmaxf(m, mc);
+        s = (s > 0.f ? s * __expf(m - mn) : 0.f) + sc * __expf(mc - mn);
+        m = mn;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float mo = __shfl_xor(m, o, WAVE), so = __shfl_xor(s, o, WAVE);
+        const float mn = fmaxf(m, mo);
+        s = (s > 0.f ? s * __expf(m - mn) : 0.f) + (so > 0.f ? so * __expf(mo - mn) : 0.f);
+        m = mn;
+    }
+    return m + logf(s);
+}
+
+// One wave per sequence.  Lane j - 1 tests draft j (j = 1..gamma) -- accept
+// iff u_j <= p_j(d_j) / q_j(d_j) -- all at once; the first failing j is the
+// rejection point (App. D.1).  work[b] then names the row of the final draw.
+__global__ void __launch_bounds__(64) k_accept_decide(rows_t r, int gamma, int V, float invT, rng_t rng,
+                                                      const int32_t* draft, const float* q_logits,
+                                                      const float* q_stats, const float* p_logits,
+                                                      const float* spart, int nch, int32_t* out_tok, int32_t* n_emit,
+                                                      float* work)
+{
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int slot = r.slots[b];
     float* wk = work + (size_t)b * WK;
     int32_t* ot = out_tok + (size_t)b * (gamma + 1);
     if (slot < 0 || slot >= r.max_slots) {
-        flag_error(r.err, ERR_SLOT);
-        for (int j = 0; j <= gamma; ++j) ot[j] = -1;
-        n_emit[b] = 0;
-        wk[0] = -1.f;
+        if (lane == 0) {
+            flag_error(r.err, ERR_SLOT);
+            n_emit[b] = 0;
+            wk[0] = -1.f;
+        }
+        for (int j = lane; j <= gamma; j += 64) ot[j] = -1;
         return;
     }
-    int kv = r.kv_len[slot];
-    int jstar = gamma + 1;
-    for (int j = 1; j <= gamma; ++j) {
-        int d = draft[(size_t)b * gamma + j - 1];
-        int prow = b * (gamma + 1) + j - 1;
-        float lsep = lse_of(spart, prow, nch);
+    const int kv = r.kv_len[slot];
+    const int prow0 = b * (gamma + 1);
+    // each lane t keeps the lse of p row t (t <= gamma); the bonus row's too
+    float my_lse = 0.f, lse_bonus = 0.f;
+    for (int t = 0; t <= gamma; ++t) {
+        const float l = wave_lse(spart, prow0 + t, nch, lane);
+        if (lane == t) my_lse = l;
+        if (t == gamma) lse_bonus = l;
+    }
+    bool reject = false;
+    int d = -1;
+    if (lane < gamma) {
+        const int j = lane + 1;
+        d = draft[(size_t)b * gamma + lane];
         float ratio = 0.f;
         if (d >= 0 && d < V) {
-            float lp = p_logits[(size_t)prow * V + d] * invT - lsep;
-            float lq = q_logits[((size_t)b * gamma + j - 1) * V + d] * invT - q_stats[((size_t)b * gamma + j - 1) * 2 + 1];
+            const float lp = p_logits[(size_t)(prow0 + lane) * V + d] * invT - my_lse;
+            const float lq = q_logits[((size_t)b * gamma + lane) * V + d] * invT - q_stats[((size_t)b * gamma + lane) * 2 + 1];
             ratio = expf(lp - lq);
         } else {
             flag_error(r.err, ERR_TOKEN);
         }
-        float u = uniform_at(rng, STREAM_ACCEPT, slot, kv + j, 0);
-        if (u <= ratio) { ot[j - 1] = d; continue; }
-        jstar = j;
-        wk[0] = 0.f; wk[1] = (float)prow; wk[2] = lsep;
-        wk[3] = q_stats[((size_t)b * gamma + j - 1) * 2 + 1];
-        wk[4] = (float)(kv + j);
-        break;
+        const float u = uniform_at(rng, STREAM_ACCEPT, slot, kv + j, 0);
+        reject = !(u <= ratio);
     }
-    if (jstar == gamma + 1) {
-        int prow = b * (gamma + 1) + gamma;
-        wk[0] = 1.f; wk[1] = (float)prow; wk[2] = lse_of(spart, prow, nch); wk[3] = 0.f;
-        wk[4] = (float)(kv + gamma + 1);
+    const uint64_t rej = __builtin_amdgcn_ballot_w64(reject);
+    const int jstar = rej ? (int)__builtin_ctzll(rej) + 1 : gamma + 1;
+    const float lse_rej = __shfl(my_lse, (jstar - 1) & 63, WAVE);
+    for (int t = lane; t <= gamma; t += 64) {
+        if (t < jstar - 1) ot[t] = d;        // t < gamma here, so lane t holds d_t
+        else if (t >= jstar) ot[t] = -1;
     }
-    wk[5] = (float)jstar;
-    for (int j = jstar; j <= gamma; ++j) ot[j] = -1;
-    n_emit[b] = jstar;
+    if (lane == 0) {
+        if (jstar <= gamma) {
+            wk[0] = 0.f; wk[1] = (float)(prow0 + jstar - 1); wk[2] = lse_rej;
+            wk[3] = q_stats[((size_t)b * gamma + jstar - 1) * 2 + 1];
+            wk[4] = (float)(kv + jstar);
+        } else {
+            wk[0] = 1.f; wk[1] = (float)(prow0 + gamma); wk[2] = lse_bonus; wk[3] = 0.f;
+            wk[4] = (float)(kv + gamma + 1);
+        }
+        wk[5] = (float)jstar;
+        n_emit[b] = jstar;
+    }
 }
 
 // final draw: residual (mode 0) or bonus (mode 1); partial per (b, chunk) =
@@ -319,8 +352,8 @@ void launch_accept(const rows_t& r, int gamma, int V, float T, rng_t rng, const 
     float invT = 1.0f / T;
     int prows = r.B * (gamma + 1);
     k_stats_partial<<<dim3(prows, nch), STHREADS, 0, s>>>(p_logits, V, invT, part, nch);
-    k_accept_decide<<<(r.B + 63) / 64, 64, 0, s>>>(r, gamma, V, invT, rng, draft, q_logits, q_stats, p_logits, part,
-                                                   nch, out_tok, n_emit, work);
+    k_accept_decide<<<r.B, 64, 0, s>>>(r, gamma, V, invT, rng, draft, q_logits, q_stats, p_logits, part, nch, out_tok,
+                                       n_emit, work);
     float* fpart = part + (size_t)prows * nch * 2;
     k_final_partial<<<dim3(r.B, nch), STHREADS, 0, s>>>(r, gamma, V, invT, rng, q_logits, p_logits, work, fpart, nch);
     k_final_combine<<<(r.B + 63) / 64, 64, 0, s>>>(r.B, gamma, work, fpart, nch, out_tok, next_tok);
