@@ -64,7 +64,7 @@ def run_rollout(cfg, W, prompt, B, ctx_target, gamma, T, seed, step, tol, ctx_fi
             assert np.all(dv["out"][n:] == -1)
             if tracked[b]:
                 r = oracle.sd_step_seq(target, drafter, okv[b], o_len[b], o_last[b], gamma, T, seed, step, b)
-                status, info = compare_step(r, dv, tol, T)
+                status, info = compare_step(r, dv, tol, T, key=(seed, step, b, o_len[b]))
                 stats["worst"] = max(stats["worst"], info.get("worst", 0.0))
                 if status == "exempt":
                     say("exempt", b, info)
@@ -145,6 +145,24 @@ def test_small_bf16_sd_matches_oracle(ctx_fill):
     say("stats", st)
     assert st["ok"] >= 3 * B
     assert st["exempt"] <= 2
+    eng.close()
+
+
+@pytest.mark.parametrize("B", [16, 48])
+def test_small_bf16_sd_verify_rows_in_one_tile(B):
+    """Batches whose verify forward has 64 < B (gamma + 1) <= 320 rows: the
+    projections and the LM head take the LDS-tiled GEMMs (split K for the
+    narrow ones)."""
+    cfg = SMALL_GQA
+    say("small bf16 SD, B", B)
+    P, gamma, T, seed = 24, 4, 1.0, 12
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
+    eng, k, v, kv_len, okv, tracked, o_len, st = run_rollout(
+        cfg, W, prompt, B, P + 12, gamma, T, seed, 5, tol=2e-2, ctx_fill=150, n_steps=2)
+    say("stats", st)
+    assert st["ok"] >= B
+    assert st["exempt"] <= max(3, B // 8)           # near-ties of the race keys (documented exemptions)
     eng.close()
 
 

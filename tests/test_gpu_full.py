@@ -61,7 +61,7 @@ def test_l4_8b_sd_step_matches_oracle_on_sampled_sequences():
         kvb = oracle.KV(cfg, cap)
         kvb.k[:, :, :S], kvb.v[:, :, :S] = ctx_host[b]
         r = oracle.sd_step_seq(target, drafter, kvb, S, int(lastn[b]), gamma, T, seed, step, b)
-        status, info = compare_step(r, rows[b], 2e-2, T)
+        status, info = compare_step(r, rows[b], 2e-2, T, key=(seed, step, b, S))
         say("sequence", b, status, info, "n_emit", r["n_emit"], rows[b]["n_emit"])
         assert status in ("ok", "exempt")
     eng.close()
