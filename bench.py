@@ -45,6 +45,9 @@ def parse():
                     help="bind a paged KV cache with pages of this many positions, shuffled (0: dense cache)")
     ap.add_argument("--graph", action="store_true",
                     help="time the SD steps as replays of one captured HIP graph")
+    ap.add_argument("--batch", type=int, default=0, help="sequences (default: the 64 of the workload)")
+    ap.add_argument("--context", type=int, default=0, help="cached positions per sequence (default 2048)")
+    ap.add_argument("--gamma", type=int, default=0, help="draft length (default 4)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -221,6 +224,7 @@ def main():
 
     cfg, run = synth.L4_8B, synth.L4_8B_RUN
     B, S, gamma, T, seed = run["B"], run["context"], run["gamma"], run["T"], run["seed"]
+    B, S, gamma = args.batch or B, args.context or S, args.gamma or gamma
     n_steps, n_warm = args.steps, args.warmup
     # every timed SD step can advance a sequence by gamma + 1 positions
     max_ctx = S + (2 * n_steps + n_warm + 2) * (gamma + 1) + args.ar_steps + gamma + 2
@@ -390,7 +394,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + "
                                + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
-                               + " drafter, B=64, KV context 2048 (random N(0,1)), gamma=4, T=1.0",
+                               + f" drafter, B={B}, KV context {S} (random N(0,1)), gamma={gamma}, T=1.0",
                    "drafter": args.drafter, "hip_graph": bool(args.graph), "kv_page_size": args.page_size,
                    "batch": B, "context": S, "gamma": gamma, "temperature": T, "layers": L, "hidden": H,
                    "heads": f"{nq}q/{nkv}kv x {d}", "ffn": F, "vocab": V},

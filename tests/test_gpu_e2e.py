@@ -166,6 +166,23 @@ def test_small_bf16_sd_verify_rows_in_one_tile(B):
     eng.close()
 
 
+@pytest.mark.parametrize("B,fmt", [(1, "w4"), (3, "w4"), (2, "w4a"), (4, "w8")])
+def test_small_bf16_sd_few_sequences(B, fmt):
+    """The tail of a batch: a few sequences (drafter GEMMs with one 32-row
+    tile mostly empty), in every drafter format."""
+    cfg = SMALL_GQA
+    say("small bf16 SD, few sequences", B, fmt)
+    P, gamma, T, seed = 24, 4, 1.0, 14
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
+    eng, k, v, kv_len, okv, tracked, o_len, st = run_rollout(
+        cfg, W, prompt, B, P + 16, gamma, T, seed, 7, tol=2e-2, ctx_fill=260, n_steps=4, fmt=fmt)
+    say("stats", st)
+    assert st["ok"] >= 2 * B
+    assert st["exempt"] <= 2
+    eng.close()
+
+
 @pytest.mark.parametrize("fmt", ["w4a", "w8"])
 def test_tiny_fp32_sd_with_other_drafter_formats(fmt):
     """The asymmetric-int4 and int8 drafters: every decision of a short
