@@ -98,8 +98,8 @@ def measured_traffic(kind: str):
 
 # the kernel each timing class brackets (bf16 KV cache, head_dim 128, M = 64 drafter rows)
 KERNEL_OF_CLASS = {
-    "attn_decode": "k_attn_mfma<128, 1>",
-    "attn_verify": "k_attn_mfma<128, 2>",
+    "attn_decode": "k_attn_mfma<128, 1, false>",
+    "attn_verify": "k_attn_mfma<128, 2, false>",
     "int4_proj": "k_gemm_q4<2, 4, 0>",
     "bf16_proj": "k_gemm_tiled<5> (qkv, o, down), k_gemm_t32<4> (gate-up)",
     "lm_head": "k_gemm_stream<2, 4> (draft rows), k_gemm_t32<4> (verify rows)",
