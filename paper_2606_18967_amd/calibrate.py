@@ -250,13 +250,13 @@ def drafter_tradeoff(cfg: dict, fmts=("w4", "w4a", "w8"), Bs=(1, 16, 64), S=2048
     return rows
 
 
-def run(cfg: dict, Bs, Ss, gammas, taus, eps=0.05, reps=8, log=print):
+def run(cfg: dict, Bs, Ss, gammas, taus, eps=0.05, reps=8, log=print, fmt: str = "w4"):
     torch_started = time.time()
     F = f_eff()
     log(f"F_eff {F / 1e12:.0f} TFLOP/s")
     base = sdrl.cost_init(cfg)
     base.F_eff = F
-    sw = Sweep(cfg, max(Bs), max(Ss), max(gammas))
+    sw = Sweep(cfg, max(Bs), max(Ss), max(gammas), fmt=fmt)
     samples, meas = [], {}
     for S in Ss:
         for B in Bs:
