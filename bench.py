@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--batch", type=int, default=0, help="sequences (default: the 64 of the workload)")
     ap.add_argument("--context", type=int, default=0, help="cached positions per sequence (default 2048)")
     ap.add_argument("--gamma", type=int, default=0, help="draft length (default 4)")
+    ap.add_argument("--model", choices=("L4_8B", "L32_8B", "L64_32B"), default="L4_8B",
+                    help="decoder: the 8B shape with 4 layers (the default workload) or 32, or the 32B shape "
+                         "with 64 layers (no CPU-oracle leg for the two large ones)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -81,14 +84,24 @@ def kernel_sources_hash(files=None):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kind: str):
+# the workload the committed counter runs time (bench.py's defaults)
+DEFAULT_WORKLOAD = "L4_8B B=64 S=2048 gamma=4 w4 page=0"
+
+
+def workload_key(model, B, S, gamma, drafter, page):
+    return f"{model} B={B} S={S} gamma={gamma} {drafter} page={page}"
+
+
+def measured_traffic(kind: str, workload: str = DEFAULT_WORKLOAD):
     """HBM bytes per launch from committed rocprofv3 counter runs, or None if
-    the kernel's sources changed since they were taken."""
+    they were taken on another workload or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
             rec = json.load(fh)
     except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload:
         return None
     d = rec.get("detail", {}).get(kind)
     if not d or d.get("sources") != kernel_sources_hash(SOURCES_OF_CLASS[kind]):
@@ -197,6 +210,7 @@ def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, out_path):
                         bytes=fetch[k][0] * 1024 * ff + write[k][0] * 1024 * wf, dispatches=fetch[k][1],
                         sources=kernel_sources_hash(SOURCES_OF_CLASS[cls]))
     rec = {
+           "workload": DEFAULT_WORKLOAD,
            "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib": fkib, "write_kib": wkib, "fetch_factor": ff,
                                 "write_factor": wf, "kernel": fname},
            "per_launch_bytes": {c: v["bytes"] for c, v in per.items()}, "detail": per}
@@ -222,7 +236,7 @@ def main():
 
     from paper_2606_18967_amd import sdrl, synth
 
-    cfg, run = synth.L4_8B, synth.L4_8B_RUN
+    cfg, run = getattr(synth, args.model), synth.L4_8B_RUN
     B, S, gamma, T, seed = run["B"], run["context"], run["gamma"], run["T"], run["seed"]
     B, S, gamma = args.batch or B, args.context or S, args.gamma or gamma
     n_steps, n_warm = args.steps, args.warmup
@@ -365,7 +379,8 @@ def main():
     else:
         achieved, peak, unit = amount / (us * 1e-6) / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
     roof = dict(bound=bound, achieved=round(achieved, 1), peak=peak, unit=unit,
-                frac=round(achieved / peak, 4), traffic=measured_traffic(dom),
+                frac=round(achieved / peak, 4),
+                traffic=measured_traffic(dom, workload_key(args.model, B, S, gamma, args.drafter, args.page_size)),
                 kernel=KERNEL_OF_CLASS.get(dom, dom), timing_class=dom,
                 algorithmic_per_launch=amount, us_per_launch=round(us, 2))
     others = {}
@@ -376,7 +391,7 @@ def main():
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
-    if not args.no_cpu_baseline and not args.page_size:
+    if not args.no_cpu_baseline and not args.page_size and args.model == "L4_8B":
         cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, args.drafter)
 
     rec = {
@@ -392,7 +407,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "8B-shaped decoder, 4 layers, bf16 target + "
+        "config": {"workload": {"L4_8B": "8B-shaped decoder, 4 layers", "L32_8B": "8B-shaped decoder, 32 layers",
+                                "L64_32B": "32B-shaped decoder, 64 layers"}[args.model] + ", bf16 target + "
                                + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
                                + f" drafter, B={B}, KV context {S} (random N(0,1)), gamma={gamma}, T=1.0",
                    "drafter": args.drafter, "hip_graph": bool(args.graph), "kv_page_size": args.page_size,

@@ -281,7 +281,7 @@ def run(cfg: dict, Bs, Ss, gammas, taus, eps=0.05, reps=8, log=print, fmt: str =
 
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--model", default="L4_8B", choices=["L4_8B", "TINY_BF16"])
+    ap.add_argument("--model", default="L4_8B", choices=["L4_8B", "L32_8B", "L64_32B", "TINY_BF16"])
     ap.add_argument("--B", default="1,4,16,64,128,256")
     ap.add_argument("--S", default="512,2048,8192")
     ap.add_argument("--gamma", default="3,7,11")
@@ -292,7 +292,7 @@ def main(argv=None):
     ap.add_argument("--drafter-tradeoff", action="store_true",
                     help="only compare the drafter formats (latency against acceptance) at S = max(--S)")
     a = ap.parse_args(argv)
-    cfg = synth.L4_8B if a.model == "L4_8B" else dict(synth.TINY, dtype="bf16", name="tiny-bf16")
+    cfg = dict(synth.TINY, dtype="bf16", name="tiny-bf16") if a.model == "TINY_BF16" else getattr(synth, a.model)
     ints = lambda s: [int(x) for x in s.split(",") if x]
     if a.drafter_tradeoff:
         rows = drafter_tradeoff(cfg, Bs=ints(a.B), S=max(ints(a.S)), gamma=max(ints(a.gamma)), reps=a.reps,
