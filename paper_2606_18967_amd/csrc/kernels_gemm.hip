@@ -514,10 +514,24 @@ void gemm_plan(int M, int N, int K, int* nbw, int* S)
 // bf16 GEMMs with more than 64 rows use the tiled kernel (N % 128 == 0).
 static bool use_tiled(int M, int N, int K) { return M > 64 && N % TBN == 0 && K % TBK == 0; }
 
-// Tile height: 160 rows when they divide M and N is small enough that the
-// splits, not the row waste, decide the time (measured on the verify shapes
-// at M = 320: qkv, o and down projections); 128 rows otherwise.
-static int tiled_mtw(int M, int N) { return (M % 160 == 0 && N <= 8192) ? 5 : 4; }
+// Tile height of the LDS-tiled kernels, in units of 32 rows: the height with
+// the fewest padded rows ceil(M / BM) BM, ties going to the taller tile, since
+// every m-tile reads the whole weight matrix again.  Heights 320, 256, 192 and
+// 128 rows are k_gemm_t32<10|8|6|4> (32x32x16 MFMAs), 160 rows k_gemm_tiled<5>
+// (16x16x32).  At M = 320 (64 sequences, gamma = 4) one 320-row tile reads each
+// weight tile once: -15% on the four projections of a layer against two 160-
+// or three 128-row tiles.
+static int tiled_mtw(int M)
+{
+    static const int cand[] = {10, 8, 6, 5, 4};
+    int best = 4;
+    long best_rows = -1;
+    for (int m : cand) {
+        const long rows = (long)((M + 32 * m - 1) / (32 * m)) * 32 * m;
+        if (best_rows < 0 || rows < best_rows) best = m, best_rows = rows;
+    }
+    return best;
+}
 
 #ifndef TILED_SPLIT_TARGET
 #define TILED_SPLIT_TARGET 192
@@ -525,7 +539,7 @@ static int tiled_mtw(int M, int N) { return (M % 160 == 0 && N <= 8192) ? 5 : 4;
 
 static void tiled_plan(int M, int N, int K, int* mtw, int* S)
 {
-    *mtw = tiled_mtw(M, N);
+    *mtw = tiled_mtw(M);
     int mtiles = (M + 32 * *mtw - 1) / (32 * *mtw);
     int tiles = N / TBN * mtiles;
     int KS = K / TBK;
@@ -569,8 +583,13 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
-        if (mtw == 5) k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
-        else k_gemm_t32<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total);
+        switch (mtw) {
+            case 10: k_gemm_t32<10><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            case 8: k_gemm_t32<8><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            case 6: k_gemm_t32<6><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            case 5: k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            default: k_gemm_t32<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+        }
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);

@@ -148,10 +148,11 @@ def test_device_range_errors_are_reported():
     eng.close()
 
 
-@pytest.mark.parametrize("M", [65, 130, 200, 320])
+@pytest.mark.parametrize("M", [65, 130, 190, 200, 320, 384, 640, 700])
 def test_dense_gemm_verify_rows(M):
-    """The bf16 GEMM at the verify forward's row counts (64 < M <= 320, the
-    LDS-tiled kernels) against torch in fp32 on the same bf16 inputs."""
+    """The bf16 GEMM at the verify forward's row counts (M > 64: the LDS-tiled
+    kernels with 128- to 320-row tiles, ragged last tiles included) against
+    torch in fp32 on the same bf16 inputs."""
     say("verify-rows gemm", M)
     g = torch.Generator(device="cuda").manual_seed(M)
     N, K = 24576, 1024
