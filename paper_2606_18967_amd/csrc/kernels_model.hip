@@ -332,7 +332,8 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 //   registers.
 //   O^T += V^T P^T: V is staged row-major in a wave-private LDS tile (row
 //   stride d + 8) and read back transposed with ds_read_b64_tr_b16.
-//   The next block's K and V are loaded while the current one computes.
+//   The next block's K and V are loaded while the current one computes (with
+//   two query tiles, the other wave on the SIMD covers the loads instead).
 // The online softmax runs per query row in base 2 with lazy rescaling (the
 // reference max of a row moves only when the block max exceeds it by more
 // than 8, bounding the exp2 terms by 256); the four waves are merged
@@ -353,9 +354,9 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 #endif
 
 // two waves per SIMD where the registers allow it without spills (one query
-// tile); the verify variants keep one
+// tile; two tiles with a single K/V register set); three or four tiles keep one
 template <int D, int MQ, bool PAGED>
-__global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
+__global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
                                                    const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch,
                                                    void* out, int out_t)
 {
@@ -573,12 +574,21 @@ __global__ void __launch_bounds__(256, MQ == 1 ? 2 : 1) k_attn_mfma(rows_t r, co
         }
     }
 
-    for (int blk = wq0; blk < wq1; blk += 2 * wstep) {
-        load_kv(blk + wstep, kf1, vv1);
-        block(blk, kf0, vv0);
-        if (blk + wstep >= wq1) break;
-        load_kv(blk + 2 * wstep, kf0, vv0);
-        block(blk + wstep, kf1, vv1);
+    if constexpr (MQ == 2) {
+        // one register set (246 VGPRs instead of 366): two waves per SIMD, the
+        // other wave hides each block's loads
+        for (int blk = wq0; blk < wq1; blk += wstep) {
+            if (blk != wq0) load_kv(blk, kf0, vv0);
+            block(blk, kf0, vv0);
+        }
+    } else {
+        for (int blk = wq0; blk < wq1; blk += 2 * wstep) {
+            load_kv(blk + wstep, kf1, vv1);
+            block(blk, kf0, vv0);
+            if (blk + wstep >= wq1) break;
+            load_kv(blk + 2 * wstep, kf0, vv0);
+            block(blk + wstep, kf1, vv1);
+        }
     }
 #pragma unroll
     for (int mt = 0; mt < MQ; ++mt) {
