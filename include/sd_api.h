@@ -230,8 +230,11 @@ sd_status sd_ar_step(sd_engine e, int32_t B, const int32_t* slots, const int32_t
  * last sd_sync (SD_E_INVAL) or HIP errors (SD_E_HIP); clears the flags. */
 sd_status sd_sync(sd_engine e, void* stream);
 
-/* Debug switch: 1 = kv_rollback poisons discarded KV with NaN. */
-sd_status sd_set_debug(sd_engine e, int32_t poison);
+/* Debug switches (flags, host): bit 0 = kv_rollback poisons discarded KV with
+ * NaN; bit 1 = the gate/up projection and SwiGLU run as two kernels (by
+ * default SwiGLU runs in the projection's epilogue where a fused kernel
+ * exists; both give identical results).  Other bits: SD_E_INVAL. */
+sd_status sd_set_debug(sd_engine e, int32_t flags);
 
 /* Kernel timing (diagnostics).  While on, the engine brackets each launch of
  * a kernel class with HIP events recorded on the launch stream.  Classes:

@@ -24,6 +24,13 @@ typedef float float2v __attribute__((ext_vector_type(2)));
 // round to nearest even (v_cvt_pk_bf16_f32); NaN stays NaN
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
+// one activation element in the GEMM input type (fp32, bf16 round-to-nearest-even, fp16)
+template <typename T>
+__device__ __forceinline__ void store_act(void* out, size_t idx, float v);
+template <> __device__ __forceinline__ void store_act<float>(void* out, size_t idx, float v) { ((float*)out)[idx] = v; }
+template <> __device__ __forceinline__ void store_act<uint16_t>(void* out, size_t idx, float v) { ((uint16_t*)out)[idx] = f32_to_bf16(v); }
+template <> __device__ __forceinline__ void store_act<_Float16>(void* out, size_t idx, float v) { ((_Float16*)out)[idx] = (_Float16)v; }
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((float2v){lo, hi}, bf16x2v));

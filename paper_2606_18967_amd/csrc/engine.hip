@@ -53,6 +53,7 @@ struct sd_engine_s {
     int dev;
     bool f32;
     int poison = 0;
+    int no_fuse = 0;             // debug: SwiGLU as its own kernel after the gate/up GEMM
     // bound (caller-owned)
     std::vector<const void*> w;
     bool weights_bound = false;
@@ -344,10 +345,12 @@ extern "C" sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages,
     return SD_OK;
 }
 
-extern "C" sd_status sd_set_debug(sd_engine e, int32_t poison)
+extern "C" sd_status sd_set_debug(sd_engine e, int32_t flags)
 {
     if (!e) return fail(SD_E_INVAL, "engine is NULL");
-    e->poison = poison != 0;
+    if (flags & ~3) return fail(SD_E_INVAL, "unknown debug flag");
+    e->poison = (flags & 1) != 0;
+    e->no_fuse = (flags & 2) != 0;
     return SD_OK;
 }
 
@@ -419,6 +422,21 @@ static int proj(sd_engine e, bool draft, int layer, int which, const void* A, fl
     return launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
 }
 
+// The gate/up projection with SwiGLU in its epilogue, writing act directly;
+// false when the shape has no fused kernel (or fusion is switched off).
+static bool proj_swiglu(sd_engine e, bool draft, int layer, const void* A, void* act, act_t at, int M, hipStream_t s)
+{
+    if (e->f32 || e->no_fuse) return false;
+    const sd_model_cfg& c = e->c;
+    if (draft) {
+        const int w = 4 * layer + PRJ_GU;
+        return launch_gemm_q4_swiglu((const uint16_t*)A, e->qw[w], e->qs[w], e->qz[w], e->qfmt, act, at, M, c.ffn,
+                                     c.hidden, s) != 0;
+    }
+    return launch_gemm_bf16_swiglu((const uint16_t*)A, (const uint16_t*)W(e, layer, 4), act, at, M, c.ffn, c.hidden,
+                                   s) != 0;
+}
+
 // One forward pass over B sequences x n tokens (row r = b*n + i at position
 // kv_len + off + i).  Token of row (b, i): i == 0 ? tokA[b*sA] :
 // tokB[b*sB + i - 1].  If logits != NULL, row r's logits go to logits + r*ldl;
@@ -445,8 +463,12 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
         if (!sp.done) { tscope t(e, T_MISC, s); launch_attention_combine(r, c.n_q, c.head_dim, e->att_part, sp, e->att, at, s); }
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
         { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }
-        { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s); }
-        { tscope t(e, T_MISC, s); launch_silu_mul(e->gu, e->gpart, S, R, c.ffn, e->act, at, s); }
+        bool fused;
+        { tscope t(e, pcls, s); fused = proj_swiglu(e, draft, l, e->a, e->act, at, R, s); }
+        if (!fused) {
+            { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_GU, e->a, e->gu, R, 2 * c.ffn, GEMM_STORE, s); }
+            { tscope t(e, T_MISC, s); launch_silu_mul(e->gu, e->gpart, S, R, c.ffn, e->act, at, s); }
+        }
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_DOWN, e->act, e->h, R, c.hidden, GEMM_ADD, s); }
         // next layer's attention norm, or the final norm (the LM head stays in the target precision)
         const bool last = l == c.n_layers - 1;

@@ -326,10 +326,14 @@ __global__ void __launch_bounds__(256) k_gemm_tiled(const uint16_t* __restrict__
 // The same tiling on v_mfma_f32_32x32x16_bf16 (MTW even): each wave's
 // (16 MTW) x 64 tile is MTW/2 x 2 blocks of 32 x 32; lane l reads row or
 // column l % 32 and k 8 (l / 32) + 0..7 of each 16-k step.
-template <int MTW>
+// SW: the SwiGLU epilogue.  W is [2F][K], gate rows then up rows; column tile
+// t loads gate rows 64t..64t+63 (waves wn = 0) and up rows F + 64t.. (wn = 1),
+// runs without split-K and writes out[m][f] = SiLU(g) u (type out_t).
+template <int MTW, bool SW>
 __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
                                                     float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
-                                                    int ldc, int mode, int S, int mtiles, int total)
+                                                    int ldc, int mode, int S, int mtiles, int total,
+                                                    void* __restrict__ out, int out_t)
 {
     constexpr int BM = 32 * MTW;
     constexpr int AP = MTW;      // 16-byte A pieces per thread per stage (BM*8/256)
@@ -357,7 +361,8 @@ __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A
 #pragma unroll
         for (int t = 0; t < WP; ++t) {
             const int pidx = tid + t * 256, row = pidx >> 3, col = (pidx & 7) * 8;
-            b[t] = *(const u32x4*)(W + (size_t)(n0 + row) * K + (size_t)kb * TBK + col);
+            const int wrow = SW ? (row < 64 ? nt * 64 + row : N / 2 + nt * 64 + row - 64) : n0 + row;
+            b[t] = *(const u32x4*)(W + (size_t)wrow * K + (size_t)kb * TBK + col);
         }
     };
     auto store = [&](int buf, const u32x4 (&a)[AP], const u32x4 (&b)[WP]) {
@@ -414,6 +419,41 @@ __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A
                 lds_barrier();
             }
         }
+    }
+    if constexpr (SW) {
+        // the up half hands its products to the gate half of the same features
+        static_assert(2 * (MTW / 2) * 2 * 16 * 64 * 4 <= sizeof(As), "SwiGLU exchange does not fit the A buffers");
+        float* ys = (float*)&As[0][0];                 // [wm][i][j][r][64 lanes]
+        auto yi = [&](int i, int j, int r) { return (((wm * (MTW / 2) + i) * 2 + j) * 16 + r) * 64 + lane; };
+        if (wn == 1) {
+#pragma unroll
+            for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) ys[yi(i, j, r)] = acc[i][j][r];
+        }
+        lds_barrier();
+        if (wn == 1) return;
+        const int F = N / 2;
+#pragma unroll
+        for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int feat = nt * 64 + 32 * j + (lane & 31);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = m0 + wm * 16 * MTW + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    if (row >= M) continue;
+                    const float g = acc[i][j][r], u = ys[yi(i, j, r)];
+                    const float v = g / (1.f + __expf(-g)) * u;
+                    const size_t oi = (size_t)row * F + feat;
+                    if (out_t == ACT_F16) store_act<_Float16>(out, oi, v);
+                    else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, v);
+                    else store_act<float>(out, oi, v);
+                }
+            }
+        return;
     }
 #pragma unroll
     for (int i = 0; i < MTW / 2; ++i)
@@ -584,11 +624,11 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
         switch (mtw) {
-            case 10: k_gemm_t32<10><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
-            case 8: k_gemm_t32<8><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
-            case 6: k_gemm_t32<6><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            case 10: k_gemm_t32<10, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0); break;
+            case 8: k_gemm_t32<8, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0); break;
+            case 6: k_gemm_t32<6, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0); break;
             case 5: k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
-            default: k_gemm_t32<4><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
+            default: k_gemm_t32<4, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0); break;
         }
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
@@ -616,6 +656,25 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
     }
     return S;
+}
+
+int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act_t out_t, int M, int F, int K,
+                            hipStream_t s)
+{
+    if (!use_tiled(M, 2 * F, K) || F % 64) return 0;
+    const int mtw = tiled_mtw(M);
+    if (mtw == 5) return 0;                              // the 16x16x32 kernel has no SwiGLU epilogue
+    const int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
+    const int total = F / 64 * mtiles;
+    dim3 grid((total + 7) / 8 * 8);
+    const int N = 2 * F;
+    switch (mtw) {
+        case 10: k_gemm_t32<10, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
+        case 8: k_gemm_t32<8, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
+        case 6: k_gemm_t32<6, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
+        default: k_gemm_t32<4, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
+    }
+    return 1;
 }
 
 void launch_gemm_f32(const float* A, const float* W, float* C, int M, int N, int K, int ldc, gemm_mode mode,

@@ -32,11 +32,6 @@ __device__ __forceinline__ bool row_geom(const rows_t& r, int row, int* b, int* 
     return *pos >= 0 && *pos < r.max_ctx;
 }
 
-template <typename T>
-__device__ __forceinline__ void store_act(void* out, size_t idx, float v);
-template <> __device__ __forceinline__ void store_act<float>(void* out, size_t idx, float v) { ((float*)out)[idx] = v; }
-template <> __device__ __forceinline__ void store_act<uint16_t>(void* out, size_t idx, float v) { ((uint16_t*)out)[idx] = f32_to_bf16(v); }
-template <> __device__ __forceinline__ void store_act<_Float16>(void* out, size_t idx, float v) { ((_Float16*)out)[idx] = (_Float16)v; }
 
 // four consecutive outputs (idx % 4 == 0) in one store
 template <typename T>

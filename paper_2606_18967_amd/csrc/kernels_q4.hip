@@ -87,12 +87,16 @@ __device__ __forceinline__ half8 dq_bytes(uint32_t w0, uint32_t w1, uint32_t mag
     return (half8){p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
 }
 
-template <int MT, int D, int FMT>
+// SW: the SwiGLU epilogue.  The weights are [2F][K], gate rows then up rows;
+// tile t takes the gate column blocks 2t, 2t + 1 (waves cb = 0, 1) and the up
+// blocks F/32 + 2t, F/32 + 2t + 1 of the same 64 features (cb = 2, 3), runs
+// without split-K, and writes out[m][f] = SiLU(g) u (type out_t) instead of C.
+template <int MT, int D, int FMT, bool SW>
 __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A, const uint32_t* __restrict__ Wq,
                                                  const uint16_t* __restrict__ Sc, const uint8_t* __restrict__ Zp,
                                                  float* __restrict__ C,
                                                  float* __restrict__ P, int M, int N, int K, int ldc, int mode,
-                                                 int S, int msup, int total)
+                                                 int S, int msup, int total, void* __restrict__ out, int out_t)
 {
     constexpr int ROWS = 32 * MT;                      // rows of one m-tile
     constexpr int AP = ROWS * 2 * (QK / 8) / 512;      // 16-byte A pieces per thread per iteration
@@ -113,7 +117,9 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
     const int G = K / QK, Gs = G / S, g0 = s * Gs, g1 = g0 + Gs;
     const int rows = min(M - m0, ROWS);
     const int nblk = N / 32;
-    const int nb = tile * 4 + cb;                      // this wave's column block (stores only if < nblk)
+    // column block of wave slot c of this tile
+    auto blk_of = [&](int c) { return SW ? (c < 2 ? tile * 2 + c : nblk / 2 + tile * 2 + c - 2) : tile * 4 + c; };
+    const int nb = blk_of(cb);                         // this wave's column block (stores only if < nblk)
     const int nbl = min(nb, nblk - 1);                 // block it loads
     const int nit = (Gs + 1) >> 1;                     // iterations (groups per k-half)
     const int nend = (nit + D - 1) / D * D;
@@ -123,12 +129,12 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
     // before the ring so that waiting for them does not wait for the ring
     const int sidx = min(tid, 16 * Gs - 1);
     const int sb = sidx / (Gs * 4), sr = sidx - sb * (Gs * 4);
-    const u32x4 sv = *(const u32x4*)(Sc + ((size_t)min(tile * 4 + sb, nblk - 1) * G + g0) * 32 + sr * 8);
+    const u32x4 sv = *(const u32x4*)(Sc + ((size_t)min(blk_of(sb), nblk - 1) * G + g0) * 32 + sr * 8);
     // zero points (asymmetric format): 4 runs of Gs*32 bytes, one 16-byte piece per thread
     const int zidx = min(tid, 8 * Gs - 1);
     const int zb = zidx / (Gs * 2), zr = zidx - zb * (Gs * 2);
     u32x4 zv = {0u, 0u, 0u, 0u};
-    if (FMT == QF_W4A) zv = *(const u32x4*)(Zp + ((size_t)min(tile * 4 + zb, nblk - 1) * G + g0) * 32 + zr * 16);
+    if (FMT == QF_W4A) zv = *(const u32x4*)(Zp + ((size_t)min(blk_of(zb), nblk - 1) * G + g0) * 32 + zr * 16);
 
     // A pieces: p = tid + 512 t -> (half, row, 16-byte column)
     u32x4 ar[D][AP];
@@ -245,6 +251,37 @@ __global__ void __launch_bounds__(512) k_gemm_q4(const uint16_t* __restrict__ A,
             for (int r = 0; r < 16; ++r) xs[((cb * MT + t) * 16 + r) * 64 + lane] = acc[t][r];
     }
     lds_barrier();
+    if constexpr (SW) {
+        // the up blocks hand their sums to the gate blocks of the same features
+        static_assert((4 + 2) * MT * 16 * 64 * 4 <= sizeof(As), "SwiGLU exchange does not fit the A buffers");
+        float* ys = xs + 4 * MT * 16 * 64;             // [2 up blocks][MT][16][64 lanes]
+        if (hh == 0) {
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    acc[t][r] += xs[((cb * MT + t) * 16 + r) * 64 + lane];
+                    if (cb >= 2) ys[(((cb - 2) * MT + t) * 16 + r) * 64 + lane] = acc[t][r];
+                }
+        }
+        lds_barrier();
+        if (hh == 1 || cb >= 2) return;
+        const int F = N / 2, feat = nb * 32 + (lane & 31);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + t * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row >= M) continue;
+                const float g = acc[t][r], u = ys[((cb * MT + t) * 16 + r) * 64 + lane];
+                const float v = g / (1.f + __expf(-g)) * u;
+                const size_t oi = (size_t)row * F + feat;
+                if (out_t == ACT_F16) store_act<_Float16>(out, oi, v);
+                else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, v);
+                else store_act<float>(out, oi, v);
+            }
+        return;
+    }
     if (hh == 1 || nb >= nblk) return;
     const int col = nb * 32 + (lane & 31);
 #pragma unroll
@@ -281,25 +318,35 @@ int q4_plan(int M, int N, int K)
     return best;
 }
 
-template <int MT, int FMT>
+template <int MT, int FMT, bool SW>
 void q4_launch_d(int D, dim3 grid, hipStream_t st, const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc,
                  const uint8_t* Z, float* C, float* P, int M, int N, int K, int ldc, int mode, int S, int msup,
-                 int total)
+                 int total, void* out, int out_t)
 {
-    if (D == 2) k_gemm_q4<MT, 2, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
-    else if (D == 3) k_gemm_q4<MT, 3, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
-    else k_gemm_q4<MT, 4, FMT><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    if (D == 2)
+        k_gemm_q4<MT, 2, FMT, SW><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
+    else if (D == 3)
+        k_gemm_q4<MT, 3, FMT, SW><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
+    else
+        k_gemm_q4<MT, 4, FMT, SW><<<grid, 512, 0, st>>>(A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
 }
 
-template <int MT>
+template <int MT, bool SW>
 void q4_launch_f(int fmt, int D, dim3 grid, hipStream_t st, const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc,
                  const uint8_t* Z, float* C, float* P, int M, int N, int K, int ldc, int mode, int S, int msup,
-                 int total)
+                 int total, void* out = nullptr, int out_t = 0)
 {
-    if (fmt == QF_W4A) q4_launch_d<MT, QF_W4A>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
-    else if (fmt == QF_W8) q4_launch_d<MT, QF_W8>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
-    else q4_launch_d<MT, QF_W4>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total);
+    if (fmt == QF_W4A)
+        q4_launch_d<MT, QF_W4A, SW>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
+    else if (fmt == QF_W8)
+        q4_launch_d<MT, QF_W8, SW>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
+    else
+        q4_launch_d<MT, QF_W4, SW>(D, grid, st, A, Wq, Sc, Z, C, P, M, N, K, ldc, mode, S, msup, total, out, out_t);
 }
+
+// ring depth (iterations in flight + 1), chosen so the padding to a multiple
+// of D wastes no iteration where possible
+int q4_ring_depth(int nit) { return nit % 4 == 0 ? 4 : (nit % 3 == 0 ? 3 : (nit >= 4 ? 4 : (nit == 3 ? 3 : 2))); }
 
 }  // namespace
 
@@ -318,13 +365,30 @@ int launch_gemm_q4(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, co
     const int S = q4_plan(M, N, K);
     if (S < 1 || (S > 1 && (size_t)S * M * N > part_cap)) return -1;
     const int G = K / QK, nit = (G / S + 1) / 2;
-    // ring depth (iterations in flight + 1), chosen so the padding to a
-    // multiple of D wastes no iteration where possible
-    const int D = nit % 4 == 0 ? 4 : (nit % 3 == 0 ? 3 : (nit >= 4 ? 4 : (nit == 3 ? 3 : 2)));
+    const int D = q4_ring_depth(nit);
     const int msup = (M + 63) / 64;
     const int total = (N / 32 + 3) / 4 * S * msup;
     dim3 grid((total + 7) / 8 * 8);
-    if (M <= 32) q4_launch_f<1>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
-    else q4_launch_f<2>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
+    if (M <= 32) q4_launch_f<1, false>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
+    else q4_launch_f<2, false>(fmt, D, grid, st, A, Wq, Sc, Z, C, part, M, N, K, ldc, mode, S, msup, total);
     return S;
+}
+
+int launch_gemm_q4_swiglu(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt,
+                          void* out, act_t out_t, int M, int F, int K, hipStream_t st)
+{
+    // one split: every group of K must fit the work-group's scale staging
+    if (K % QK || F % 64 || K / QK > QSMAX || M < 1 || fmt < QF_W4 || fmt > QF_W8 || (fmt == QF_W4A && !Z)) return 0;
+    const int G = K / QK, nit = (G + 1) / 2;
+    const int D = q4_ring_depth(nit);
+    const int msup = (M + 63) / 64;
+    const int total = F / 64 * msup;
+    dim3 grid((total + 7) / 8 * 8);
+    if (M <= 32)
+        q4_launch_f<1, true>(fmt, D, grid, st, A, Wq, Sc, Z, nullptr, nullptr, M, 2 * F, K, 0, 0, 1, msup, total, out,
+                             (int)out_t);
+    else
+        q4_launch_f<2, true>(fmt, D, grid, st, A, Wq, Sc, Z, nullptr, nullptr, M, 2 * F, K, 0, 0, 1, msup, total, out,
+                             (int)out_t);
+    return 1;
 }

@@ -164,3 +164,34 @@ def test_dense_gemm_verify_rows(M):
     torch.cuda.synchronize()
     err = (out - ref).abs().max().item()
     assert err <= 1e-4 * ref.abs().max().item(), err
+
+
+@pytest.mark.parametrize("fmt", ["w4", "w4a", "w8"])
+@pytest.mark.parametrize("B", [3, 16, 64])
+def test_fused_swiglu_equals_separate_kernel(B, fmt):
+    """SwiGLU in the gate/up GEMM's epilogue (int4 drafter GEMM with one or two
+    32-row tiles; the tiled bf16 verify GEMM at 80 and 320 rows) gives the
+    same SD step, bit for bit, as the gate/up GEMM followed by the SwiGLU
+    kernel: same fp32 sums, same SiLU."""
+    say("fused swiglu", B, fmt)
+    cfg = SMALL_BF16
+    gamma, T, seed, S = 4, 1.0, 31, 48
+    W = [w.cuda() for w in synth.make_weights(cfg, 13, "cpu")]
+    eng, k, v, kv_len = make_engine(cfg, W, B, S + gamma + 4, gamma, fmt=fmt)
+    synth.fill_kv_context(k, v, S, 17)
+    slots = torch.arange(B, dtype=torch.int32, device="cuda")
+    last = synth.make_tokens(B, 1, cfg["vocab"], 19)[:, 0].cuda().contiguous()
+    outs = []
+    for unfused in (False, True):
+        eng.set_debug(False, unfused_swiglu=unfused)
+        kv_len.fill_(S)
+        bufs = sdrl.SDBuffers(eng, B, gamma)
+        sdrl.sd_step(eng, bufs, slots, last, T, seed, 1)
+        eng.sync()
+        outs.append([t.cpu() for t in (bufs.draft_tok, bufs.q_logits, bufs.p_logits, bufs.out_tok, bufs.n_emit,
+                                       k[:, :, :, S:S + gamma + 1].contiguous(), v[:, :, :, S:S + gamma + 1].contiguous())])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    with pytest.raises(sdrl.SDError, match="debug flag"):
+        sdrl._check(sdrl.lib().sd_set_debug(eng.h, 4))
+    eng.close()
