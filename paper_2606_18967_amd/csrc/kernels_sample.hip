@@ -22,6 +22,7 @@ namespace {
 
 constexpr int SCHUNK = 4096;            // vocabulary entries per work-group
 constexpr int STHREADS = 256;
+static_assert(SCHUNK % (8 * STHREADS) == 0, "a chunk is whole Philox blocks per thread");
 
 struct philox_out { uint64_t w[4]; };
 
@@ -100,23 +101,52 @@ __global__ void __launch_bounds__(STHREADS) k_sample_partial(rows_t r, const flo
     bool ok = slot >= 0 && slot < r.max_slots;
     int pos = ok ? r.kv_len[slot] + pos_off : 0;
     const float* lr = logits + (size_t)b * ld;
-    race_t v = {-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-    int i0 = ch * SCHUNK;
-    for (int blk = (i0 >> 3) + threadIdx.x; blk * 8 < min(i0 + SCHUNK, V); blk += STHREADS) {
-        philox_out o = philox4x64_10((uint64_t)blk, (uint64_t)(uint32_t)pos, (uint64_t)(uint32_t)slot,
-                                     (uint64_t)STREAM_TOKEN, rng.seed, rng.step);
+    // the thread's Philox blocks (8 consecutive entries each) in registers,
+    // 16-byte loads where a block is whole and aligned; then max, sum of
+    // exponentials and the race, with no data-dependent branch on the values
+    constexpr int NB = SCHUNK / 8 / STHREADS;
+    const int i0 = ch * SCHUNK;
+    const bool vec = ((uintptr_t)lr & 15) == 0;
+    float x[NB][8], key[NB][8];
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+        const int blk = (i0 >> 3) + threadIdx.x + STHREADS * bb;
+        const philox_out o = philox4x64_10((uint64_t)blk, (uint64_t)(uint32_t)pos, (uint64_t)(uint32_t)slot,
+                                           (uint64_t)STREAM_TOKEN, rng.seed, rng.step);
+        if (vec && blk * 8 + 8 <= V) {
+            const float4 a = *(const float4*)(lr + blk * 8), c = *(const float4*)(lr + blk * 8 + 4);
+            x[bb][0] = a.x; x[bb][1] = a.y; x[bb][2] = a.z; x[bb][3] = a.w;
+            x[bb][4] = c.x; x[bb][5] = c.y; x[bb][6] = c.z; x[bb][7] = c.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[bb][e] = blk * 8 + e < V ? lr[blk * 8 + e] : -INFINITY;
+        }
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            int i = blk * 8 + e;
-            if (i >= V) break;
-            uint64_t w = o.w[e >> 1];
-            float u = u_of((e & 1) ? (uint32_t)(w >> 32) : (uint32_t)w);
-            float x = lr[i] * invT;
-            float key = x + gumbel(u);
-            if (x > v.m) { v.s = v.s * __expf(v.m - x) + 1.f; v.m = x; }
-            else v.s += __expf(x - v.m);
-            if (better(key, i, v.key, v.idx)) { v.key = key; v.idx = i; }
+            const uint64_t w = o.w[e >> 1];
+            const float u = u_of((e & 1) ? (uint32_t)(w >> 32) : (uint32_t)w);
+            const bool live = blk * 8 + e < V && blk * 8 + e < i0 + SCHUNK;
+            x[bb][e] = live ? x[bb][e] * invT : -INFINITY;
+            key[bb][e] = live ? x[bb][e] + gumbel(u) : -INFINITY;
         }
+    }
+    race_t v = {-INFINITY, 0.f, -INFINITY, 0x7fffffff};
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v.m = fmaxf(v.m, x[bb][e]);
+    if (v.m > -INFINITY) {
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v.s += __expf(x[bb][e] - v.m);
+    }
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+        const int blk = (i0 >> 3) + threadIdx.x + STHREADS * bb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (better(key[bb][e], blk * 8 + e, v.key, v.idx)) { v.key = key[bb][e]; v.idx = blk * 8 + e; }
     }
     v = block_race(v, sh);
     if (threadIdx.x == 0) {
@@ -145,19 +175,40 @@ __global__ void k_sample_combine(rows_t r, const float* part, int nch, int32_t* 
 
 // ------------------------------------------------------------------ row statistics
 // partial (max, sumexp) of logits/T for rows of a [rows][V] block
+// Each thread holds its SCHUNK / STHREADS entries in registers (16-byte loads
+// when the chunk is whole and aligned), takes their max, then sums the
+// exponentials with no data-dependent branch.
 __global__ void __launch_bounds__(STHREADS) k_stats_partial(const float* logits, int V, float invT, float* part,
                                                             int nch)
 {
+    constexpr int PER = SCHUNK / STHREADS;
     __shared__ race_t sh[STHREADS / 64];
-    int row = blockIdx.x, ch = blockIdx.y;
+    const int row = blockIdx.x, ch = blockIdx.y;
     const float* lr = logits + (size_t)row * V;
-    race_t v = {-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-    int i1 = min((ch + 1) * SCHUNK, V);
-    for (int i = ch * SCHUNK + threadIdx.x; i < i1; i += STHREADS) {
-        float x = lr[i] * invT;
-        if (x > v.m) { v.s = v.s * __expf(v.m - x) + 1.f; v.m = x; }
-        else v.s += __expf(x - v.m);
+    const int i0 = ch * SCHUNK;
+    float x[PER];
+    if (i0 + SCHUNK <= V && ((uintptr_t)(lr + i0) & 15) == 0) {
+#pragma unroll
+        for (int t = 0; t < PER / 4; ++t) {
+            const float4 f = *(const float4*)(lr + i0 + 4 * (threadIdx.x + STHREADS * t));
+            x[4 * t] = f.x * invT; x[4 * t + 1] = f.y * invT; x[4 * t + 2] = f.z * invT; x[4 * t + 3] = f.w * invT;
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < PER; ++t) {
+            const int i = i0 + threadIdx.x + STHREADS * t;
+            x[t] = i < V ? lr[i] * invT : -INFINITY;
+        }
     }
+    float m = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < PER; ++t) m = fmaxf(m, x[t]);
+    float sum = 0.f;
+    if (m > -INFINITY) {
+#pragma unroll
+        for (int t = 0; t < PER; ++t) sum += __expf(x[t] - m);
+    }
+    race_t v = {m, sum, -INFINITY, 0x7fffffff};
     v = block_race(v, sh);
     if (threadIdx.x == 0) { part[((size_t)row * nch + ch) * 2] = v.m; part[((size_t)row * nch + ch) * 2 + 1] = v.s; }
 }
