@@ -327,23 +327,49 @@ __global__ void __launch_bounds__(STHREADS) k_final_partial(rows_t r, int gamma,
     const float* lp = p_logits + (size_t)prow * V;
     const float* lq = q_logits + ((size_t)b * gamma + min(jstar, gamma) - 1) * V;   // read in mode 0 only
     int stream = mode == 0 ? STREAM_RESIDUAL : STREAM_TOKEN;
+    // the thread's Philox blocks in registers (16-byte loads where a block is
+    // whole and aligned), then both races; the mode is uniform per work-group
+    constexpr int NB = SCHUNK / 8 / STHREADS;
+    const int i0 = ch * SCHUNK;
+    const bool vec = (((uintptr_t)lp | (uintptr_t)lq) & 15) == 0;
+    float xp[NB][8], xq[NB][8];
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+        const int base = ((i0 >> 3) + threadIdx.x + STHREADS * bb) * 8;
+        if (vec && base + 8 <= V) {
+            const float4 a = *(const float4*)(lp + base), c = *(const float4*)(lp + base + 4);
+            xp[bb][0] = a.x; xp[bb][1] = a.y; xp[bb][2] = a.z; xp[bb][3] = a.w;
+            xp[bb][4] = c.x; xp[bb][5] = c.y; xp[bb][6] = c.z; xp[bb][7] = c.w;
+            if (mode == 0) {
+                const float4 d = *(const float4*)(lq + base), f = *(const float4*)(lq + base + 4);
+                xq[bb][0] = d.x; xq[bb][1] = d.y; xq[bb][2] = d.z; xq[bb][3] = d.w;
+                xq[bb][4] = f.x; xq[bb][5] = f.y; xq[bb][6] = f.z; xq[bb][7] = f.w;
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                xp[bb][e] = base + e < V ? lp[base + e] : 0.f;
+                if (mode == 0) xq[bb][e] = base + e < V ? lq[base + e] : 0.f;
+            }
+        }
+    }
     race_t va = {0.f, 0.f, -INFINITY, 0x7fffffff}, vb = va;
-    int i0 = ch * SCHUNK;
-    for (int blk = (i0 >> 3) + threadIdx.x; blk * 8 < min(i0 + SCHUNK, V); blk += STHREADS) {
-        philox_out o = philox4x64_10((uint64_t)blk, (uint64_t)(uint32_t)pos, (uint64_t)(uint32_t)slot,
-                                     (uint64_t)stream, rng.seed, rng.step);
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+        const int blk = (i0 >> 3) + threadIdx.x + STHREADS * bb;
+        const philox_out o = philox4x64_10((uint64_t)blk, (uint64_t)(uint32_t)pos, (uint64_t)(uint32_t)slot,
+                                           (uint64_t)stream, rng.seed, rng.step);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            int i = blk * 8 + e;
-            if (i >= V) break;
-            uint64_t w = o.w[e >> 1];
-            float g = gumbel(u_of((e & 1) ? (uint32_t)(w >> 32) : (uint32_t)w));
-            float xp = lp[i] * invT;
-            float kb = xp + g;
+            const int i = blk * 8 + e;
+            const uint64_t w = o.w[e >> 1];
+            const float g = gumbel(u_of((e & 1) ? (uint32_t)(w >> 32) : (uint32_t)w));
+            const float x = xp[bb][e] * invT;
+            const float kb = i < V ? x + g : -INFINITY;
             float ka = kb;
             if (mode == 0) {
-                float rr = expf(xp - lsep) - expf(lq[i] * invT - lseq);
-                ka = rr > 0.f ? logf(rr) + g : -INFINITY;
+                const float rr = expf(x - lsep) - expf(xq[bb][e] * invT - lseq);
+                ka = rr > 0.f && i < V ? logf(rr) + g : -INFINITY;
             }
             if (better(ka, i, va.key, va.idx)) { va.key = ka; va.idx = i; }
             if (better(kb, i, vb.key, vb.idx)) { vb.key = kb; vb.idx = i; }
