@@ -233,7 +233,9 @@ sd_status sd_sync(sd_engine e, void* stream);
 /* Debug switches (flags, host): bit 0 = kv_rollback poisons discarded KV with
  * NaN; bit 1 = the gate/up projection and SwiGLU run as two kernels (by
  * default SwiGLU runs in the projection's epilogue where a fused kernel
- * exists; both give identical results).  Other bits: SD_E_INVAL. */
+ * exists); bit 2 = bf16 GEMMs with 320-row tiles stage their operands through
+ * registers instead of loading them into LDS by DMA.  Each switch gives
+ * identical results.  Other bits: SD_E_INVAL. */
 sd_status sd_set_debug(sd_engine e, int32_t flags);
 
 /* Kernel timing (diagnostics).  While on, the engine brackets each launch of

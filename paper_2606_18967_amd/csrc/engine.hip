@@ -54,6 +54,7 @@ struct sd_engine_s {
     bool f32;
     int poison = 0;
     int no_fuse = 0;             // debug: SwiGLU as its own kernel after the gate/up GEMM
+    int no_dma = 0;              // debug: register-staged 320-row GEMM tiles instead of the DMA-fed ones
     // bound (caller-owned)
     std::vector<const void*> w;
     bool weights_bound = false;
@@ -348,9 +349,10 @@ extern "C" sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages,
 extern "C" sd_status sd_set_debug(sd_engine e, int32_t flags)
 {
     if (!e) return fail(SD_E_INVAL, "engine is NULL");
-    if (flags & ~3) return fail(SD_E_INVAL, "unknown debug flag");
+    if (flags & ~7) return fail(SD_E_INVAL, "unknown debug flag");
     e->poison = (flags & 1) != 0;
     e->no_fuse = (flags & 2) != 0;
+    e->no_dma = (flags & 4) != 0;
     return SD_OK;
 }
 
@@ -419,7 +421,8 @@ static int proj(sd_engine e, bool draft, int layer, int which, const void* A, fl
     }
     const void* w = W(e, layer, widx[which]);
     if (e->f32) { launch_gemm_f32((const float*)A, (const float*)w, C, M, N, K, ldc, mode, s); return 1; }
-    return launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s);
+    return launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)w, C, e->gpart, e->gpart_cap, M, N, K, ldc, mode, true, s,
+                            !e->no_dma);
 }
 
 // The gate/up projection with SwiGLU in its epilogue, writing act directly;
@@ -434,7 +437,7 @@ static bool proj_swiglu(sd_engine e, bool draft, int layer, const void* A, void*
                                      c.hidden, s) != 0;
     }
     return launch_gemm_bf16_swiglu((const uint16_t*)A, (const uint16_t*)W(e, layer, 4), act, at, M, c.ffn, c.hidden,
-                                   s) != 0;
+                                   s, !e->no_dma) != 0;
 }
 
 // One forward pass over B sequences x n tokens (row r = b*n + i at position
@@ -480,7 +483,7 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
         tscope t(e, T_LMHEAD, s);
         if (e->f32) launch_gemm_f32((const float*)e->a, (const float*)e->w[2], logits, R, c.vocab, c.hidden, (int)ldl, GEMM_STORE, s);
         else launch_gemm_bf16((const uint16_t*)e->a, (const uint16_t*)e->w[2], logits, e->gpart, e->gpart_cap, R, c.vocab,
-                                c.hidden, (int)ldl, GEMM_STORE, false, s);
+                                c.hidden, (int)ldl, GEMM_STORE, false, s, !e->no_dma);
     }
 }
 

@@ -74,16 +74,18 @@ enum gemm_mode : int { GEMM_STORE = 0, GEMM_ADD = 1 };
 // kernel for M > 64.  part is split-K scratch of part_cap floats (no split
 // when too small).  Returns the number of K splits S used.  With
 // defer_reduce and S > 1 the partials are left in part ([S][M][N]) for the
-// consumer to sum; otherwise C holds the result.
+// consumer to sum; otherwise C holds the result.  lds_dma: 320-row tiles
+// without split-K use the DMA-fed kernel (same sums as the register-staged
+// one; false selects the latter).
 int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part, size_t part_cap, int M, int N, int K,
-                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s);
+                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s, bool lds_dma = true);
 // The gate/up projection with SwiGLU in its epilogue: out[M][F] (type out_t)
 // = SiLU(g) * u, [g | u] = A W^T with W [2F][K] (gate rows, then up rows).
 // Returns 1 when launched, 0 when the shape has no fused kernel (the caller
 // then runs the plain GEMM and launch_silu_mul).  The int4 form takes the
 // packed drafter layout of kernels_q4.hip.
 int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act_t out_t, int M, int F, int K,
-                            hipStream_t s);
+                            hipStream_t s, bool lds_dma = true);
 int launch_gemm_q4_swiglu(const uint16_t* A, const uint32_t* Wq, const uint16_t* Sc, const uint8_t* Z, int fmt,
                           void* out, act_t out_t, int M, int F, int K, hipStream_t s);
 size_t gemm_part_floats(int M, int N, int K);

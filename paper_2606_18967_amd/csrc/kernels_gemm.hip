@@ -474,6 +474,158 @@ __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A
         }
 }
 
+// ------------------------------------------------------------------ 320-row tiles fed by LDS DMA
+// The 320-row tile of k_gemm_t32 (wave tile 160 x 64, v_mfma_f32_32x32x16_bf16,
+// the same MFMA operands in the same k order, so the same fp32 sums) with the
+// operands brought into LDS by global_load_lds_dwordx4: each instruction puts
+// 64 lanes x 16 bytes straight into 1 KB of LDS, so no registers stage the
+// tiles and the waves issue no LDS stores.  K advances in stages of 64 through
+// two LDS buffers: stage k + 1 is requested right after the barrier that opens
+// stage k.  A stage holds 128-byte rows (64 k) of the A and W tiles; the
+// 16-byte chunk c of row r sits at position c ^ sw(r), sw(r) = (r ^ r / 8) % 8,
+// which keeps the fragment reads (rows r..r+7 or r..r+15 at one chunk) free of
+// bank conflicts; a DMA lane therefore fetches chunk pos ^ sw(r) of its row.
+// WN = 2: 320 x 128 tiles, 4 waves; WN = 4: 320 x 256 tiles, 8 waves (half the
+// activation re-reads per weight byte, for launches with a full wave of tiles).
+// SW: the SwiGLU epilogue; the tile takes 64 features, and wave column wn's
+// two 32-column blocks are the gate rows and the up rows of the same 32
+// features, so SiLU(g) u is formed in registers.  No split-K.
+constexpr int DBK = 64, DRB = DBK * 2;                  // k per stage, bytes per tile row
+
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_byte)
+{
+    asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(src), "{m0}"(lds_byte) : "memory");
+}
+
+// s_waitcnt vmcnt(N) with the other counters left free (gfx9 field layout)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ int dma_sw(int r) { return (r ^ (r >> 3)) & 7; }
+
+template <int WN, bool SW>
+__global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+                                                       float* __restrict__ C, int M, int N, int K, int ldc, int mode,
+                                                       int mtiles, int total, void* __restrict__ out, int out_t)
+{
+    constexpr int MTW = 10, BM = 32 * MTW, BN = 64 * WN, NWAVE = 2 * WN;
+    constexpr int NA = BM / 8, NI = NA + BN / 8;               // 1 KB pieces (8 rows) per stage
+    constexpr int STG = (BM + BN) * DRB;
+    constexpr int CNT = NI / NWAVE;                            // pieces per wave per stage
+    static_assert(NI % NWAVE == 0, "every wave issues the same number of pieces");
+    static_assert(!SW || WN == 2, "the SwiGLU form uses 64-feature tiles");
+    __shared__ __attribute__((aligned(1024))) uint8_t sm[2 * STG];
+    const uint32_t sbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sm;
+    const int per_xcd = gridDim.x >> 3;
+    const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (w >= total) return;
+    const int mt = w % mtiles, nt = w / mtiles;
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wv / WN, wn = wv % WN;
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int Ks = K / DBK;
+    const int rows = min(M - m0, BM);
+
+    // this lane's source row and chunk for each of its pieces
+    const uint16_t* src[CNT];
+    uint32_t dst[CNT];
+#pragma unroll
+    for (int q = 0; q < CNT; ++q) {
+        const int t = wv + q * NWAVE, rl = lane >> 3, pos = lane & 7;
+        if (t < NA) {
+            const int row = 8 * t + rl;
+            src[q] = A + (size_t)(m0 + min(row, rows - 1)) * K + 8 * (pos ^ dma_sw(row));
+            dst[q] = t * 1024;
+        } else {
+            const int row = 8 * (t - NA) + rl;
+            int wrow = n0 + row;
+            if constexpr (SW) {
+                const int f = nt * 64 + (row >> 6) * 32 + (row & 31);   // wave column row/64, block (row/32)%2
+                wrow = ((row >> 5) & 1) ? N / 2 + f : f;
+            }
+            src[q] = W + (size_t)wrow * K + 8 * (pos ^ dma_sw(row));
+            dst[q] = BM * DRB + (t - NA) * 1024;
+        }
+    }
+    auto issue = [&](int buf, int kb) {
+#pragma unroll
+        for (int q = 0; q < CNT; ++q) lds_dma16(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+    };
+
+    floatx16 acc[MTW / 2][2];
+#pragma unroll
+    for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    issue(0, 0);
+    for (int kb = 0; kb < Ks; ++kb) {
+        wait_vmcnt<0>();                    // this wave's pieces of stage kb are in LDS
+        lds_barrier();                      // everyone's are, and stage kb - 1 is no longer read
+        if (kb + 1 < Ks) issue((kb + 1) & 1, kb + 1);
+        const uint8_t* sa = sm + (kb & 1) * STG;
+        const uint8_t* sw = sa + BM * DRB;
+#pragma unroll
+        for (int ks = 0; ks < DBK / 16; ++ks) {
+            const int c = 2 * ks + (lane >> 5);
+            u32x4 af[MTW / 2], bw[2];
+#pragma unroll
+            for (int i = 0; i < MTW / 2; ++i) {
+                const int r = wm * 16 * MTW + 32 * i + (lane & 31);
+                af[i] = *(const u32x4*)(sa + r * DRB + ((c ^ dma_sw(r)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int r = wn * 64 + 32 * j + (lane & 31);
+                bw[j] = *(const u32x4*)(sw + r * DRB + ((c ^ dma_sw(r)) << 4));
+            }
+#pragma unroll
+            for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[i]),
+                                                                       __builtin_bit_cast(bf16x8, bw[j]), acc[i][j],
+                                                                       0, 0, 0);
+        }
+    }
+    if constexpr (SW) {
+        const int F = N / 2, feat = nt * 64 + wn * 32 + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 16 * MTW + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row >= M) continue;
+                const float g = acc[i][0][r], u = acc[i][1][r];
+                const float v = g / (1.f + __expf(-g)) * u;
+                const size_t oi = (size_t)row * F + feat;
+                if (out_t == ACT_F16) store_act<_Float16>(out, oi, v);
+                else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, v);
+                else store_act<float>(out, oi, v);
+            }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < MTW / 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = n0 + wn * 64 + 32 * j + (lane & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 16 * MTW + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row >= M) continue;
+                float* cp = C + (size_t)row * ldc + col;
+                *cp = mode == GEMM_ADD ? *cp + acc[i][j][r] : acc[i][j][r];
+            }
+        }
+}
+
 // C[m][n] (+)= sum_s P[s][m][n]
 __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__ P, float* __restrict__ C, int M, int N,
                                                        int ldc, int S, int mode)
@@ -614,13 +766,23 @@ static void stream_mt(int MT, dim3 grid, hipStream_t s, const uint16_t* A, const
 }
 
 int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part, size_t part_cap, int M, int N, int K,
-                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s)
+                     int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s, bool lds_dma)
 {
     if (use_tiled(M, N, K)) {
         int mtw, S;
         tiled_plan(M, N, K, &mtw, &S);
         if (S > 1 && (size_t)S * M * N > part_cap) S = 1;
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
+        if (lds_dma && mtw == 10 && S == 1) {
+            // 320-row tiles without split-K: the DMA-fed kernel, 256 columns
+            // per tile when that still gives a full wave of work-groups
+            const bool wide = N % 256 == 0 && N / 256 * mtiles >= 256;
+            const int total = N / (wide ? 256 : 128) * mtiles;
+            dim3 grid((total + 7) / 8 * 8);
+            if (wide) k_gemm_dma<4, false><<<grid, 512, 0, s>>>(A, W, C, M, N, K, ldc, mode, mtiles, total, nullptr, 0);
+            else k_gemm_dma<2, false><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, mode, mtiles, total, nullptr, 0);
+            return 1;
+        }
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
         switch (mtw) {
@@ -659,7 +821,7 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
 }
 
 int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act_t out_t, int M, int F, int K,
-                            hipStream_t s)
+                            hipStream_t s, bool lds_dma)
 {
     if (!use_tiled(M, 2 * F, K) || F % 64) return 0;
     const int mtw = tiled_mtw(M);
@@ -668,6 +830,10 @@ int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act
     const int total = F / 64 * mtiles;
     dim3 grid((total + 7) / 8 * 8);
     const int N = 2 * F;
+    if (lds_dma && mtw == 10) {
+        k_gemm_dma<2, true><<<grid, 256, 0, s>>>(A, W, nullptr, M, N, K, 0, 0, mtiles, total, out, out_t);
+        return 1;
+    }
     switch (mtw) {
         case 10: k_gemm_t32<10, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
         case 8: k_gemm_t32<8, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;

@@ -254,8 +254,9 @@ class Engine:
         self.drafter_fmt = fmt
         return qbuf
 
-    def set_debug(self, poison: bool, unfused_swiglu: bool = False):
-        _check(lib().sd_set_debug(self.h, (1 if poison else 0) | (2 if unfused_swiglu else 0)))
+    def set_debug(self, poison: bool, unfused_swiglu: bool = False, staged_tiles: bool = False):
+        _check(lib().sd_set_debug(self.h, (1 if poison else 0) | (2 if unfused_swiglu else 0) |
+                                  (4 if staged_tiles else 0)))
 
     # ---------------------------------------------------------------- steps
     def _slots(self, slots):

@@ -148,14 +148,32 @@ def test_device_range_errors_are_reported():
     eng.close()
 
 
-@pytest.mark.parametrize("M", [65, 130, 190, 200, 320, 384, 640, 700])
+@pytest.mark.parametrize("M", [65, 130, 190, 200, 300, 320, 384, 600, 640, 700])
 def test_dense_gemm_verify_rows(M):
     """The bf16 GEMM at the verify forward's row counts (M > 64: the LDS-tiled
-    kernels with 128- to 320-row tiles, ragged last tiles included) against
-    torch in fp32 on the same bf16 inputs."""
+    kernels with 128- to 320-row tiles, ragged last tiles included; 300, 320,
+    600 and 640 rows take the DMA-fed 320-row tiles, 128 columns wide at this
+    N) against torch in fp32 on the same bf16 inputs."""
     say("verify-rows gemm", M)
     g = torch.Generator(device="cuda").manual_seed(M)
     N, K = 24576, 1024
+    A = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    W = torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)
+    out = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    sdrl.dense_gemm_bf16(A, W, out)
+    ref = A.float() @ W.float().t()
+    torch.cuda.synchronize()
+    err = (out - ref).abs().max().item()
+    assert err <= 1e-4 * ref.abs().max().item(), err
+
+
+@pytest.mark.parametrize("M", [300, 320])
+def test_dense_gemm_wide_dma_tiles(M):
+    """N with at least 256 tiles of 256 columns: the DMA-fed 320 x 256 tiles
+    (eight waves), as used by the verify LM head, against torch in fp32."""
+    say("wide dma gemm", M)
+    g = torch.Generator(device="cuda").manual_seed(M + 1)
+    N, K = 65536, 512
     A = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
     W = torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)
     out = torch.empty((M, N), dtype=torch.float32, device="cuda")
@@ -193,5 +211,37 @@ def test_fused_swiglu_equals_separate_kernel(B, fmt):
     for a, b in zip(*outs):
         assert torch.equal(a, b)
     with pytest.raises(sdrl.SDError, match="debug flag"):
-        sdrl._check(sdrl.lib().sd_set_debug(eng.h, 4))
+        sdrl._check(sdrl.lib().sd_set_debug(eng.h, 8))
+    eng.close()
+
+
+@pytest.mark.parametrize("fmt", ["w4", "w8"])
+@pytest.mark.parametrize("B", [52, 64])
+def test_dma_fed_tiles_equal_register_staged_tiles(B, fmt):
+    """The verify forward's 320-row GEMM tiles loaded into LDS by DMA (all four
+    projections, SwiGLU fused, and the LM head) give the same SD step, bit
+    for bit, as the register-staged tiles: the same MFMA operands in the same
+    k order.  B = 52 leaves 60 of the 320 rows empty."""
+    say("dma-fed tiles", B, fmt)
+    cfg = SMALL_BF16
+    gamma, T, seed, S = 4, 1.0, 37, 40
+    W = [w.cuda() for w in synth.make_weights(cfg, 23, "cpu")]
+    eng, k, v, kv_len = make_engine(cfg, W, B, S + gamma + 4, gamma, fmt=fmt)
+    synth.fill_kv_context(k, v, S, 29)
+    slots = torch.arange(B, dtype=torch.int32, device="cuda")
+    last = synth.make_tokens(B, 1, cfg["vocab"], 31)[:, 0].cuda().contiguous()
+    outs = []
+    for staged in (False, True):
+        for unfused in (False, True):
+            eng.set_debug(False, unfused_swiglu=unfused, staged_tiles=staged)
+            kv_len.fill_(S)
+            bufs = sdrl.SDBuffers(eng, B, gamma)
+            sdrl.sd_step(eng, bufs, slots, last, T, seed, 1)
+            eng.sync()
+            outs.append([t.cpu() for t in (bufs.p_logits, bufs.out_tok, bufs.n_emit,
+                                           k[:, :, :, S:S + gamma + 1].contiguous(),
+                                           v[:, :, :, S:S + gamma + 1].contiguous())])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert torch.equal(a, b)
     eng.close()
