@@ -489,7 +489,8 @@ __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A
 // activation re-reads per weight byte, for launches with a full wave of tiles).
 // SW: the SwiGLU epilogue; the tile takes 64 features, and wave column wn's
 // two 32-column blocks are the gate rows and the up rows of the same 32
-// features, so SiLU(g) u is formed in registers.  No split-K.
+// features, so SiLU(g) u is formed in registers (no split-K there).  With S
+// K splits the partial sums go to P[s][M][N] as in k_gemm_t32.
 constexpr int DBK = 64, DRB = DBK * 2;                  // k per stage, bytes per tile row
 
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_byte)
@@ -509,8 +510,9 @@ __device__ __forceinline__ int dma_sw(int r) { return (r ^ (r >> 3)) & 7; }
 
 template <int WN, bool SW>
 __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
-                                                       float* __restrict__ C, int M, int N, int K, int ldc, int mode,
-                                                       int mtiles, int total, void* __restrict__ out, int out_t)
+                                                       float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
+                                                       int ldc, int mode, int S, int mtiles, int total,
+                                                       void* __restrict__ out, int out_t)
 {
     constexpr int MTW = 10, BM = 32 * MTW, BN = 64 * WN, NWAVE = 2 * WN;
     constexpr int NA = BM / 8, NI = NA + BN / 8;               // 1 KB pieces (8 rows) per stage
@@ -523,11 +525,12 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
     const int per_xcd = gridDim.x >> 3;
     const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     if (w >= total) return;
-    const int mt = w % mtiles, nt = w / mtiles;
+    const int mt = w % mtiles, rest = w / mtiles;
+    const int s = rest % S, nt = rest / S;
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wv / WN, wn = wv % WN;
     const int m0 = mt * BM, n0 = nt * BN;
-    const int Ks = K / DBK;
+    const int Ks = K / DBK / S, k0 = s * Ks;
     const int rows = min(M - m0, BM);
 
     // this lane's source row and chunk for each of its pieces
@@ -538,7 +541,7 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
         const int t = wv + q * NWAVE, rl = lane >> 3, pos = lane & 7;
         if (t < NA) {
             const int row = 8 * t + rl;
-            src[q] = A + (size_t)(m0 + min(row, rows - 1)) * K + 8 * (pos ^ dma_sw(row));
+            src[q] = A + (size_t)(m0 + min(row, rows - 1)) * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
             dst[q] = t * 1024;
         } else {
             const int row = 8 * (t - NA) + rl;
@@ -547,7 +550,7 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
                 const int f = nt * 64 + (row >> 6) * 32 + (row & 31);   // wave column row/64, block (row/32)%2
                 wrow = ((row >> 5) & 1) ? N / 2 + f : f;
             }
-            src[q] = W + (size_t)wrow * K + 8 * (pos ^ dma_sw(row));
+            src[q] = W + (size_t)wrow * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
             dst[q] = BM * DRB + (t - NA) * 1024;
         }
     }
@@ -620,8 +623,12 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
             for (int r = 0; r < 16; ++r) {
                 const int row = m0 + wm * 16 * MTW + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 if (row >= M) continue;
-                float* cp = C + (size_t)row * ldc + col;
-                *cp = mode == GEMM_ADD ? *cp + acc[i][j][r] : acc[i][j][r];
+                if (S == 1) {
+                    float* cp = C + (size_t)row * ldc + col;
+                    *cp = mode == GEMM_ADD ? *cp + acc[i][j][r] : acc[i][j][r];
+                } else {
+                    P[((size_t)s * M + row) * N + col] = acc[i][j][r];
+                }
             }
         }
 }
@@ -773,15 +780,21 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         tiled_plan(M, N, K, &mtw, &S);
         if (S > 1 && (size_t)S * M * N > part_cap) S = 1;
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
-        if (lds_dma && mtw == 10 && S == 1) {
-            // 320-row tiles without split-K: the DMA-fed kernel, 256 columns
-            // per tile when that still gives a full wave of work-groups
-            const bool wide = N % 256 == 0 && N / 256 * mtiles >= 256;
-            const int total = N / (wide ? 256 : 128) * mtiles;
+        if (lds_dma && mtw == 10) {
+            // 320-row tiles: the DMA-fed kernel, 256 columns per tile when
+            // that still gives a full wave of work-groups without split-K
+            const bool wide = S == 1 && N % 256 == 0 && N / 256 * mtiles >= 256;
+            const int total = N / (wide ? 256 : 128) * mtiles * S;
             dim3 grid((total + 7) / 8 * 8);
-            if (wide) k_gemm_dma<4, false><<<grid, 512, 0, s>>>(A, W, C, M, N, K, ldc, mode, mtiles, total, nullptr, 0);
-            else k_gemm_dma<2, false><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, mode, mtiles, total, nullptr, 0);
-            return 1;
+            if (wide)
+                k_gemm_dma<4, false><<<grid, 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, 1, mtiles, total, nullptr, 0);
+            else
+                k_gemm_dma<2, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0);
+            if (S > 1 && !defer_reduce) {
+                size_t MN = (size_t)M * N;
+                k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
+            }
+            return S;
         }
         int total = N / TBN * mtiles * S;
         dim3 grid((total + 7) / 8 * 8);
@@ -831,7 +844,7 @@ int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act
     dim3 grid((total + 7) / 8 * 8);
     const int N = 2 * F;
     if (lds_dma && mtw == 10) {
-        k_gemm_dma<2, true><<<grid, 256, 0, s>>>(A, W, nullptr, M, N, K, 0, 0, mtiles, total, out, out_t);
+        k_gemm_dma<2, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t);
         return 1;
     }
     switch (mtw) {
