@@ -114,8 +114,8 @@ KERNEL_OF_CLASS = {
     "attn_decode": "k_attn_mfma<128, 1, false>",
     "attn_verify": "k_attn_mfma<128, 2, false>",
     "int4_proj": "k_gemm_q4<2, 4, 0, false> (qkv, down; gate/up runs as the SwiGLU variant <2, 4, 0, true>)",
-    "bf16_proj": "k_gemm_t32<10, false> (qkv, o, down; gate/up runs as the SwiGLU variant <10, true>)",
-    "lm_head": "k_gemm_stream<2, 4, 8> (draft rows), k_gemm_t32<10, false> (verify rows)",
+    "bf16_proj": "k_gemm_dma<2, false> (qkv, o, down; gate/up runs as the SwiGLU variant <2, true>)",
+    "lm_head": "k_gemm_stream<2, 4, 8> (draft rows), k_gemm_dma<4, false> (verify rows)",
 }
 
 
@@ -202,9 +202,9 @@ def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, out_path):
 
     ff, fname, fkib = copy_factor(copy_fetch_csv, "FETCH_SIZE")
     wf, wname, wkib = copy_factor(copy_write_csv, "WRITE_SIZE")
-    # the 320-row tiled kernel also runs the verify LM head (about 1000
-    # work-groups); the projections' class keeps its own launches (<= 512)
-    keep = {"k_gemm_t32<10,false>": lambda wgs: wgs <= 512}
+    # the projections' class keeps its own launches of the 128-column DMA
+    # kernel (<= 512 work-groups at 320 rows)
+    keep = {"k_gemm_dma<2,false>": lambda wgs: wgs <= 512}
     fetch = per_kernel(fetch_csv, "FETCH_SIZE", keep)
     write = per_kernel(write_csv, "WRITE_SIZE", keep)
     per = {}
