@@ -155,21 +155,30 @@ __global__ void __launch_bounds__(STHREADS) k_sample_partial(rows_t r, const flo
     }
 }
 
-__global__ void k_sample_combine(rows_t r, const float* part, int nch, int32_t* tok, int tok_stride, float* stats,
-                                 int stats_stride)
+// one wave per row: lane c merges chunks c, c + 64, ..., then a butterfly
+__global__ void __launch_bounds__(64) k_sample_combine(rows_t r, const float* part, int nch, int32_t* tok,
+                                                       int tok_stride, float* stats, int stats_stride)
 {
-    int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= r.B) return;
+    const int b = blockIdx.x, lane = threadIdx.x;
     const float* p = part + (size_t)b * nch * 4;
-    race_t v = {p[0], p[1], p[2], __float_as_int(p[3])};
-    for (int c = 1; c < nch; ++c) {
-        race_t t = {p[c * 4], p[c * 4 + 1], p[c * 4 + 2], __float_as_int(p[c * 4 + 3])};
+    race_t v = {-INFINITY, 0.f, -INFINITY, 0x7fffffff};
+    for (int c = lane; c < nch; c += 64) {
+        const race_t t = {p[c * 4], p[c * 4 + 1], p[c * 4 + 2], __float_as_int(p[c * 4 + 3])};
         race_merge(v, t);
     }
-    tok[(size_t)b * tok_stride] = v.idx;
-    if (stats) {
-        stats[(size_t)b * stats_stride] = v.m;
-        stats[(size_t)b * stats_stride + 1] = v.m + logf(v.s);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        race_t t;
+        t.m = __shfl_xor(v.m, o, WAVE); t.s = __shfl_xor(v.s, o, WAVE);
+        t.key = __shfl_xor(v.key, o, WAVE); t.idx = __shfl_xor(v.idx, o, WAVE);
+        race_merge(v, t);
+    }
+    if (lane == 0) {
+        tok[(size_t)b * tok_stride] = v.idx;
+        if (stats) {
+            stats[(size_t)b * stats_stride] = v.m;
+            stats[(size_t)b * stats_stride + 1] = v.m + logf(v.s);
+        }
     }
 }
 
@@ -383,26 +392,38 @@ __global__ void __launch_bounds__(STHREADS) k_final_partial(rows_t r, int gamma,
     }
 }
 
-__global__ void k_final_combine(int B, int gamma, const float* work, const float* part, int nch, int32_t* out_tok,
-                                int32_t* next_tok)
+// one wave per sequence, as k_sample_combine
+__global__ void __launch_bounds__(64) k_final_combine(int gamma, const float* work, const float* part, int nch,
+                                                      int32_t* out_tok, int32_t* next_tok)
 {
-    int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= B) return;
+    const int b = blockIdx.x, lane = threadIdx.x;
     const float* wk = work + (size_t)b * WK;
-    if (wk[0] < 0.f) { if (next_tok) next_tok[b] = -1; return; }
+    if (wk[0] < 0.f) {
+        if (next_tok && lane == 0) next_tok[b] = -1;
+        return;
+    }
     const float* p = part + (size_t)b * nch * 4;
     float ka = -INFINITY, kb = -INFINITY;
     int ia = 0x7fffffff, ib = 0x7fffffff;
-    for (int c = 0; c < nch; ++c) {
+    for (int c = lane; c < nch; c += 64) {
         float k = p[c * 4]; int i = __float_as_int(p[c * 4 + 1]);
         if (better(k, i, ka, ia)) { ka = k; ia = i; }
         k = p[c * 4 + 2]; i = __float_as_int(p[c * 4 + 3]);
         if (better(k, i, kb, ib)) { kb = k; ib = i; }
     }
-    int y = ka > -INFINITY ? ia : ib;
-    int jstar = (int)wk[5];
-    out_tok[(size_t)b * (gamma + 1) + jstar - 1] = y;
-    if (next_tok) next_tok[b] = y;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        float k = __shfl_xor(ka, o, WAVE); int i = __shfl_xor(ia, o, WAVE);
+        if (better(k, i, ka, ia)) { ka = k; ia = i; }
+        k = __shfl_xor(kb, o, WAVE); i = __shfl_xor(ib, o, WAVE);
+        if (better(k, i, kb, ib)) { kb = k; ib = i; }
+    }
+    if (lane == 0) {
+        const int y = ka > -INFINITY ? ia : ib;
+        const int jstar = (int)wk[5];
+        out_tok[(size_t)b * (gamma + 1) + jstar - 1] = y;
+        if (next_tok) next_tok[b] = y;
+    }
 }
 
 }  // namespace
@@ -418,7 +439,7 @@ void launch_sample(const rows_t& r, const float* logits, long ld, int V, float T
 {
     int nch = sample_chunks(V);
     k_sample_partial<<<dim3(r.B, nch), STHREADS, 0, s>>>(r, logits, ld, V, 1.0f / T, rng, pos_off, part, nch);
-    k_sample_combine<<<(r.B + 63) / 64, 64, 0, s>>>(r, part, nch, tok, tok_stride, stats, stats_stride);
+    k_sample_combine<<<r.B, 64, 0, s>>>(r, part, nch, tok, tok_stride, stats, stats_stride);
 }
 
 void launch_accept(const rows_t& r, int gamma, int V, float T, rng_t rng, const int32_t* draft,
@@ -433,5 +454,5 @@ void launch_accept(const rows_t& r, int gamma, int V, float T, rng_t rng, const 
                                        n_emit, work);
     float* fpart = part + (size_t)prows * nch * 2;
     k_final_partial<<<dim3(r.B, nch), STHREADS, 0, s>>>(r, gamma, V, invT, rng, q_logits, p_logits, work, fpart, nch);
-    k_final_combine<<<(r.B + 63) / 64, 64, 0, s>>>(r.B, gamma, work, fpart, nch, out_tok, next_tok);
+    k_final_combine<<<r.B, 64, 0, s>>>(gamma, work, fpart, nch, out_tok, next_tok);
 }
