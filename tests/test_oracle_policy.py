@@ -13,8 +13,13 @@
   - App. F.3: the gamma schedules 5->7->9->11 (Qwen2.5-7B, tau 5.73, 7.60,
     9.48), 5->7->9 (Qwen2.5-14B, 5.73, 7.61), and Llama3.1-8B holding at 5
     with tau ~ 5.5; no lowering at gamma_low.
-Model shapes are the public architectures of the three checkpoints.
+The printed values are the fixtures under tests/golden/ (each file names its
+table or section).  Model shapes are the public architectures of the three
+checkpoints.
 """
+import json
+import pathlib
+
 import numpy as np
 import pytest
 
@@ -26,14 +31,15 @@ MODELS = {  # L, hidden, n_q, n_kv, head_dim, ffn, vocab
     "llama3.1-8b": (32, 4096, 32, 8, 128, 14336, 128256),
 }
 
-TABLE3 = {  # (S, B): FFN, QKVO, Attn, LM head, Nonlinear (percent)
-    "qwen2.5-7b": {(2048, 8): (75.2, 10.9, 6.2, 7.2, 0.5), (2048, 4): (77.8, 11.2, 3.2, 7.4, 0.3),
-                   (4096, 2): (77.9, 11.2, 3.2, 7.4, 0.2), (8192, 1): (78.0, 11.2, 3.2, 7.5, 0.1)},
-    "qwen2.5-14b": {(2048, 8): (65.0, 19.3, 10.3, 5.0, 0.4), (2048, 4): (68.7, 20.4, 5.4, 5.2, 0.2),
-                    (4096, 2): (68.8, 20.4, 5.4, 5.3, 0.1), (8192, 1): (68.8, 20.4, 5.4, 5.3, 0.1)},
-    "llama3.1-8b": {(2048, 8): (65.4, 15.6, 12.4, 6.1, 0.5), (2048, 4): (69.9, 16.7, 6.7, 6.5, 0.3),
-                    (4096, 2): (70.0, 16.7, 6.7, 6.5, 0.2), (8192, 1): (70.0, 16.7, 6.7, 6.5, 0.1)},
-}
+GOLDEN = pathlib.Path(__file__).parent / "golden"
+
+
+def golden(name):
+    return json.loads((GOLDEN / name).read_text())
+
+
+TABLE3 = {m: {tuple(int(x) for x in k.split(",")): tuple(v) for k, v in rows.items()}
+          for m, rows in golden("table3_decode_breakdown.json")["rows"].items()}
 
 
 @pytest.mark.parametrize("model", list(MODELS))
@@ -45,9 +51,10 @@ def test_table3_decode_breakdown(model):
 
 
 def test_table4_idealized_draft_ratio():
-    for dbits, printed in ((4, 0.360), (8, 0.573)):
-        c = oracle.cost_arch(*MODELS["qwen2.5-7b"], dbits=dbits, BW_eff=1.0, F_eff=1e30)
-        tp, tq, tv = oracle.cost_times(c, 1, 2048, 5)
+    g = golden("table4_draft_ratio.json")
+    for dbits, printed in ((int(k), v) for k, v in g["ratio"].items()):
+        c = oracle.cost_arch(*MODELS[g["model"]], dbits=dbits, BW_eff=1.0, F_eff=1e30)
+        tp, tq, tv = oracle.cost_times(c, g["B"], g["S"], 5)
         assert abs(tq / tp - printed) <= 0.003, (dbits, tq / tp)
 
 
@@ -72,9 +79,8 @@ def test_tau_alpha_closed_form_and_inverse():
             assert oracle.alpha_from_tau(oracle.tau_from_alpha(alpha, gamma), gamma) == pytest.approx(alpha, abs=1e-9)
 
 
-@pytest.mark.parametrize("tau,gamma,alpha_pct", [
-    (7.5, 7, 98.2), (5.6, 5, 97.3), (5.5, 5, 96.3), (2.1, 3, 57.3), (5.4, 5, 95.8),
-])
+@pytest.mark.parametrize("tau,gamma,alpha_pct",
+                         [(r["tau"], r["gamma"], r["alpha_pct"]) for r in golden("table2_tau_alpha.json")["rows"]])
 def test_table2_alpha_from_tau(tau, gamma, alpha_pct):
     # tau is printed to one decimal: the printed alpha must lie in the image of [tau-0.05, tau+0.05]
     lo = 100 * oracle.alpha_from_tau(tau - 0.05, gamma)
@@ -82,26 +88,35 @@ def test_table2_alpha_from_tau(tau, gamma, alpha_pct):
     assert lo - 0.05 <= alpha_pct <= hi + 0.05, (lo, hi)
 
 
-GSET = [5, 7, 9, 11]
+F3 = golden("appf3_gamma_schedules.json")
+GSET = F3["gamma_set"]
 
 
 def _schedule(taus):
     out, hist, g = [], [], GSET[0]
     for t in taus:
         hist.append(t)
-        g = oracle.gamma_next(GSET, g, hist, P=2, a_up=0.94, a_down=0.85)
+        g = oracle.gamma_next(GSET, g, hist, P=F3["P"], a_up=F3["alpha_up"], a_down=F3["alpha_down"])
         out.append(g)
     return out
 
 
 def test_app_f3_gamma_schedules():
-    # Qwen2.5-7B: tau reaches 5.73, 7.60, 9.48 before each raise
-    assert _schedule([5.0, 5.73, 5.73, 7.37, 7.60, 7.60, 9.35, 9.48, 9.48, 11.25]) == \
-        [5, 5, 7, 7, 7, 9, 9, 9, 11, 11]
-    # Qwen2.5-14B: 5.73 and 7.61
-    assert _schedule([5.73, 5.73, 7.61, 7.61])[-1] == 9
-    # Llama3.1-8B: tau improves from 5.07 to ~5.5 and never crosses 1 + 5*0.94 = 5.70
-    assert _schedule([5.07, 5.2, 5.3, 5.5, 5.5, 5.5]) == [5] * 6
+    # Qwen2.5-7B: each printed tau, held for the window of P = 2 steps, raises gamma; the tau reached
+    # after a raise stays below the next threshold until the next printed tau
+    q7 = F3["raises"]["qwen2.5-7b"]
+    taus, want = [5.0], [5]
+    for r in q7:
+        taus += [r["tau"], r["tau"], r["tau_after"]]
+        want += [r["from"], r["to"], r["to"]]
+    assert _schedule(taus) == want
+    # Qwen2.5-14B: 5 -> 7 -> 9 at its printed taus
+    q14 = F3["raises"]["qwen2.5-14b"]
+    taus = [x for r in q14 for x in (r["tau"], r["tau"])]
+    assert _schedule(taus)[1::2] == [r["to"] for r in q14]
+    # Llama3.1-8B: tau improves from 5.07 to its printed ~5.5 and never crosses 1 + 5*0.94 = 5.70
+    hold = F3["holds"]["llama3.1-8b"]
+    assert _schedule([5.07, 5.2, 5.3, hold["tau_max"], hold["tau_max"], hold["tau_max"]]) == [hold["gamma"]] * 6
     # the raise needs the minimum of the window at or above 1 + gamma*alpha_up
     assert _schedule([5.705, 5.705])[-1] == 7 and _schedule([5.695, 5.71])[-1] == 5
     # lowering: max of the window <= 1 + gamma*alpha_down, never below gamma_low
