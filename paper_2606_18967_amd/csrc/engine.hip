@@ -120,6 +120,21 @@ struct tscope {
     }
 };
 
+// Times exactly one kernel: the events are handed to the launch, which binds
+// them to the kernel's own dispatch, so their elapsed time is the kernel's
+// run time with no launch gap (the figure rocprofv3's kernel trace reports).
+struct kscope {
+    hipEvent_t start = nullptr, stop = nullptr;
+    kscope(sd_engine e, int cls)
+    {
+        if (!e->timing) return;
+        start = tscope::next_event(e);
+        stop = tscope::next_event(e);
+        if (!start || !stop) { start = stop = nullptr; return; }
+        e->marks[cls].push_back({start, stop});
+    }
+};
+
 static void prj_shape(const sd_model_cfg& c, int which, int* N, int* K)
 {
     int qkvN = (c.n_q + 2 * c.n_kv) * c.head_dim;
@@ -462,7 +477,8 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
         { tscope t(e, T_MISC, s); launch_rope_kv(r, e->qkv, e->gpart, S, e->rope, c.n_q, kv, l, e->qrot, s); }
         if (!logits && l == c.n_layers - 1) break;      // the rest of the last layer only feeds the logits
         attn_split sp;
-        { tscope t(e, n == 1 ? T_ATTN_D : T_ATTN_V, s); sp = launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s); }
+        { kscope t(e, n == 1 ? T_ATTN_D : T_ATTN_V);
+          sp = launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s, t.start, t.stop); }
         if (!sp.done) { tscope t(e, T_MISC, s); launch_attention_combine(r, c.n_q, c.head_dim, e->att_part, sp, e->att, at, s); }
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
         { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }

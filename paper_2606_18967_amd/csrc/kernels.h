@@ -56,8 +56,11 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, co
 // chunks and chunk length of a split-context attention launch; done when
 // each sequence was a single chunk and the kernel wrote the output itself
 struct attn_split { int chunks, chunk; bool done; };
+// ev0/ev1, when given, are bound to the attention kernel's own dispatch
+// (hipExtLaunchKernelGGL): their elapsed time is the kernel's run time.
 attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, void* out, act_t out_t, hipStream_t s);
+                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0 = nullptr,
+                            hipEvent_t ev1 = nullptr);
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
                               act_t out_t, hipStream_t s);
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks);

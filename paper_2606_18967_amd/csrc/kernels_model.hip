@@ -3,6 +3,7 @@
 //
 // Row convention of every forward call: row r = b*n + i is token i of
 // sequence b, at absolute position kv_len[slots[b]] + off + i.
+#include <hip/hip_ext.h>
 #include "common.h"
 #include "kernels.h"
 
@@ -786,23 +787,35 @@ size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks)
     return (size_t)R * n_q * max_chunks * (head_dim + 2);
 }
 
+// a launch whose events (if any) are bound to the kernel's dispatch
+template <typename F, typename... Args>
+static void launch_ev(F kern, dim3 grid, dim3 block, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, Args... args)
+{
+    if (ev0) hipExtLaunchKernelGGL(kern, grid, block, 0, s, ev0, ev1, 0, args...);
+    else kern<<<grid, block, 0, s>>>(args...);
+}
+
 template <int D, bool PAGED>
-static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, const rows_t& r, const float* q, int n_q,
-                             const cache_t& c, int layer, float* part, int mch, int ch, void* out, int out_t)
+static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const rows_t& r,
+                             const float* q, int n_q, const cache_t& c, int layer, float* part, int mch, int ch,
+                             void* out, int out_t)
 {
     const uint16_t* kc = (const uint16_t*)c.k;
     const uint16_t* vc = (const uint16_t*)c.v;
+    auto go = [&](auto kern) {
+        launch_ev(kern, grid, dim3(256), s, ev0, ev1, r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t);
+    };
     switch (MQ) {
-        case 1: k_attn_mfma<D, 1, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
-        case 2: k_attn_mfma<D, 2, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
-        case 3: k_attn_mfma<D, 3, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
-        default: k_attn_mfma<D, 4, PAGED><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t); break;
+        case 1: go(k_attn_mfma<D, 1, PAGED>); break;
+        case 2: go(k_attn_mfma<D, 2, PAGED>); break;
+        case 3: go(k_attn_mfma<D, 3, PAGED>); break;
+        default: go(k_attn_mfma<D, 4, PAGED>); break;
     }
 }
 
 template <typename T, int D>
 static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                         int max_chunks, void* out, act_t out_t, hipStream_t s)
+                         int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
 {
     if constexpr (sizeof(T) == 2) {
         // bf16 cache: MFMA kernel.  max_chunks (the partial buffer's chunk
@@ -822,26 +835,26 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
         dim3 grid(r.B * c.n_kv, mch, zs);
         // one chunk per sequence: the kernel writes the final output itself
         void* o = mch == 1 ? out : nullptr;
-        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch, o, out_t);
-        else attn_mfma_launch<D, false>(MQ, grid, s, r, q, n_q, c, layer, part, mch, ch, o, out_t);
+        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t);
+        else attn_mfma_launch<D, false>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t);
         return attn_split{mch, ch, o != nullptr};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
-        k_attn_partial<T, D><<<grid, 256, 0, s>>>(r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v, c.g, layer, part,
-                                                  max_chunks);
+        launch_ev(k_attn_partial<T, D>, grid, dim3(256), s, ev0, ev1, r, q, n_q, c.n_kv, (const T*)c.k, (const T*)c.v,
+                  c.g, layer, part, max_chunks);
         return attn_split{max_chunks, ATT_CH, false};
     }
 }
 
 attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, void* out, act_t out_t, hipStream_t s)
+                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
 {
     if (c.head_dim == 128) {
-        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
-        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
+        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
     }
-    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
-    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s);
+    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
+    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
 }
 
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
