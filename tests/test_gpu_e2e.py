@@ -102,10 +102,11 @@ def test_tiny_fp32_sd_rollout_matches_oracle():
     eng.close()
 
 
-def test_tiny_fp32_ar_matches_oracle():
+@pytest.mark.parametrize("T", [1.0, 0.5, 1.6])
+def test_tiny_fp32_ar_matches_oracle(T):
     cfg, run = synth.TINY, synth.TINY_RUN
-    say("tiny fp32 AR")
-    B, P, T, seed, step = run["B"], run["prompt"], 1.0, 4, 8
+    say("tiny fp32 AR", T)
+    B, P, seed, step = run["B"], run["prompt"], 4, 8
     W = synth.make_weights(cfg, seed, "cpu")
     prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
     eng, k, v, kv_len = make_engine(cfg, [w.cuda() for w in W], B, 128, 4)
@@ -129,6 +130,24 @@ def test_tiny_fp32_ar_matches_oracle():
     eng.close()
 
 
+
+@pytest.mark.parametrize("gamma,T", [(1, 1.0), (7, 1.0), (4, 0.6), (4, 1.7), (2, 0.35)])
+def test_tiny_fp32_sd_matches_oracle_over_gamma_and_temperature(gamma, T):
+    """The SD path at the shortest draft, a long draft, and away from T = 1
+    (logits scaled by 1/T in the draft draws, the accept test, the residual
+    and bonus draws): every decision of a short rollout of the tiny fp32 model
+    against the oracle, token for token."""
+    cfg, run = synth.TINY, synth.TINY_RUN
+    say("tiny fp32 SD", gamma, T)
+    seed = 40 + gamma
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(run["B"], run["prompt"], cfg["vocab"], seed)
+    eng, *_, st = run_rollout(cfg, W, prompt, run["B"], run["prompt"] + 24, gamma, T, seed, 5, tol=5e-3, n_steps=8)
+    say("stats", st)
+    assert st["ok"] >= 3 * run["B"] and st["exempt"] <= 1
+    eng.close()
+
+
 SMALL_GQA = dict(name="small-gqa-bf16", n_layers=2, hidden=512, n_q=4, n_kv=2, head_dim=128, ffn=1024,
                  vocab=2048, dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
 
@@ -144,6 +163,22 @@ def test_small_bf16_sd_matches_oracle(ctx_fill):
         cfg, W, prompt, B, P + 24, gamma, T, seed, 11, tol=2e-2, ctx_fill=ctx_fill, n_steps=4)
     say("stats", st)
     assert st["ok"] >= 3 * B
+    assert st["exempt"] <= 2
+    eng.close()
+
+
+@pytest.mark.parametrize("gamma,T", [(3, 0.7), (6, 1.4)])
+def test_small_bf16_sd_matches_oracle_away_from_unit_temperature(gamma, T):
+    """The bf16 path (int4 drafter, GQA, head_dim 128) at other draft lengths
+    and temperatures, after 300 positions of random context."""
+    cfg = SMALL_GQA
+    say("small bf16 SD", gamma, T)
+    B, P, seed = 8, 40, 16
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
+    eng, *_, st = run_rollout(cfg, W, prompt, B, P + 24, gamma, T, seed, 13, tol=2e-2, ctx_fill=300, n_steps=3)
+    say("stats", st)
+    assert st["ok"] >= 2 * B
     assert st["exempt"] <= 2
     eng.close()
 

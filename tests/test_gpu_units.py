@@ -143,6 +143,17 @@ def test_device_range_errors_are_reported():
     with pytest.raises(ValueError):
         eng.verify(i32([0]), i32([1]), torch.zeros((1, 2), dtype=torch.int32, device="cuda"), 2,
                    torch.zeros((1, 2, cfg["vocab"]), device="cuda"))
+    # temperature must be finite and > 0; gamma at least 1
+    o1, l1 = torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros((1, cfg["vocab"]), device="cuda")
+    for bad_T in (0.0, -1.0, float("nan"), float("inf")):
+        with pytest.raises(sdrl.SDError, match="temperature"):
+            eng.ar_step(i32([0]), i32([1]), bad_T, 0, 0, o1, l1)
+        with pytest.raises(sdrl.SDError, match="temperature"):
+            eng.draft(i32([0]), i32([1]), 2, bad_T, 0, 0, torch.zeros((1, 2), dtype=torch.int32, device="cuda"),
+                      torch.zeros((1, 2, cfg["vocab"]), device="cuda"), torch.zeros((1, 2, 2), device="cuda"))
+    with pytest.raises((sdrl.SDError, ValueError)):
+        eng.draft(i32([0]), i32([1]), 0, 1.0, 0, 0, torch.zeros((1, 0), dtype=torch.int32, device="cuda"),
+                  torch.zeros((1, 0, cfg["vocab"]), device="cuda"), torch.zeros((1, 0, 2), device="cuda"))
     kv_len.zero_()
     eng.sync()
     eng.close()
