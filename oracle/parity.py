@@ -12,7 +12,12 @@ seeded generators and from its own earlier outputs).  Rules:
            nearly equal keys and the sequence stops being compared);
   accept   accept / reject decisions must be identical unless
            |u - p/q| < 1e-3 at the deciding position; the final residual or
-           bonus draw follows the draw rule.
+           bonus draw follows the draw rule.  A decision or draw that still
+           differs is judged on identical logits: the oracle's accept (the
+           rejection rule of App. D.1) run on the device's own p and q must
+           reproduce the device's tokens exactly.  The difference then comes
+           only from logit differences within the tolerance, which move p/q
+           (an accept test) or the race of the residual max(0, p - q).
 """
 from __future__ import annotations
 
@@ -65,16 +70,19 @@ def compare_step(r: dict, dev: dict, tol: float, T: float = 1.0, key=None):
         delta = float(np.abs(dev["p"] - r["p"]).max() + np.abs(dev["q"] - r["q"]).max()) / T
         if r["final_gap"] <= 2 * delta + 1e-6:
             return "exempt", dict(where="final draw", gap=r["final_gap"], delta=delta)
-        # The residual max(0, p - q) of the rejection rule (App. D.1) is the
-        # difference of two nearly equal distributions wherever the drafter
-        # agrees with the target, so logit differences within the tolerance
-        # can move its race.  Such a draw is checked by running the oracle's
-        # accept on the device's own logits: it must give the device's tokens.
-        if key is not None and n_d <= gamma:
-            seed, step, slot, kv_len = key
-            n2, out2, *_ = oracle.accept_seq(dev["draft"], dev["q"], dev["p"], T, seed, step, slot, kv_len)
-            if n2 == n_d and np.array_equal(out2[:n2], out_d):
-                return "exempt", dict(where="residual draw", note="oracle on device logits agrees")
+    # Judged on identical logits: the residual max(0, p - q) of the rejection
+    # rule (App. D.1) is the difference of two nearly equal distributions
+    # wherever the drafter agrees with the target, and p/q of an accept test
+    # moves with the logits, so logit differences within the tolerance can
+    # change either.  The oracle's accept on the device's own logits must then
+    # give the device's tokens exactly.
+    if key is not None:
+        seed, step, slot, kv_len = key
+        n2, out2, *_ = oracle.accept_seq(dev["draft"], dev["q"], dev["p"], T, seed, step, slot, kv_len)
+        if n2 == n_d and np.array_equal(out2[:n2], out_d):
+            where = "residual draw" if n_d == n_o else f"accept {k}"
+            return "exempt", dict(where=where, note="oracle on device logits agrees", u=float(r["u"][k - 1]) if k <= gamma else None,
+                                  ratio=float(r["ratio"][k - 1]) if k <= gamma else None)
     raise Mismatch(f"accept: dev n={n_d} out={out_d.tolist()} oracle n={n_o} out={r['out'].tolist()} "
                    f"u={r['u'].tolist()} ratio={r['ratio'].tolist()}")
 

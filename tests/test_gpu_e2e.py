@@ -201,6 +201,24 @@ def test_small_bf16_sd_verify_rows_in_one_tile(B):
     eng.close()
 
 
+@pytest.mark.parametrize("B", [96, 130])
+def test_small_bf16_sd_batches_past_one_m_tile(B):
+    """Batches of more than 64 sequences: the drafter GEMM runs two or three
+    64-row m-tiles (a ragged last one at 130), and the verify forward has 480
+    and 650 rows, so its GEMMs take several tiles and the LM head of each draft
+    step takes the LDS-tiled kernel."""
+    cfg = SMALL_GQA
+    say("small bf16 SD, B", B)
+    P, gamma, T, seed = 24, 4, 1.0, 19
+    W = synth.make_weights(cfg, seed, "cpu")
+    prompt = synth.make_tokens(B, P, cfg["vocab"], seed)
+    eng, *_, st = run_rollout(cfg, W, prompt, B, P + 12, gamma, T, seed, 9, tol=2e-2, ctx_fill=150, n_steps=2)
+    say("stats", st)
+    assert st["ok"] >= B
+    assert st["exempt"] <= max(3, B // 8)
+    eng.close()
+
+
 @pytest.mark.parametrize("B,fmt", [(1, "w4"), (3, "w4"), (2, "w4a"), (4, "w8")])
 def test_small_bf16_sd_few_sequences(B, fmt):
     """The tail of a batch: a few sequences (drafter GEMMs with one 32-row
