@@ -226,20 +226,21 @@ def tau_at(tau: float, gamma_meas: int, gamma: int) -> float:
     return float(sdrl.tau_from_alpha(sdrl.alpha_from_tau(tau, gamma_meas), gamma))
 
 
-def train(run_fn, policy: str, n_steps: int, lengths_fn, gset=GAMMA_SET, P=PATIENCE, a_up=A_UP, a_down=A_DOWN):
+def train(run_fn, policy: str, n_steps: int, lengths_fn, gset=GAMMA_SET, P=PATIENCE, a_up=A_UP, a_down=A_DOWN,
+          tau_carry: bool = False):
     """n_steps training steps of Algorithm 1 under one policy: gamma_1 =
     gamma_low and tau_0 = gamma_low; after each rollout the measured tau_t
     becomes the toggle's tau for the next step and (policy 'adaptive')
     drives gamma_{t+1}.  A rollout with no SD iteration measures no tau; the
     previous one is kept and the controller is not stepped.
 
-    The toggle prices SD at the step's draft length gamma_t, and the block
-    efficiency in its speedup is the one at that draft length; when the
-    adaptive policy has just changed gamma, the tau measured at the old
-    length is carried to the new one through the acceptance rate (tau_at).
-    Taken literally, a tau measured at a shorter draft would price the longer
-    draft's extra drafting against the shorter draft's gain, the toggle could
-    stay off, and with no SD iteration no new tau would ever be measured.
+    By default the toggle of step t gets the measured tau_{t-1} as it is,
+    together with gamma_t, as Algorithm 1 writes it.  With tau_carry, a tau
+    measured at another draft length is first carried to gamma_t through
+    the acceptance rate (tau_at): the speedup of eq:sd_speedup_toggle uses
+    the block efficiency at the draft length it prices, and a tau measured
+    at a shorter draft understates the longer draft's gain.  The two
+    variants differ only in the step after gamma moves.
 
     run_fn(policy, gamma, tau_prev, lengths, step) returns a RolloutResult."""
     ctl = sdrl.GammaController(gset, P, a_up, a_down)
@@ -247,7 +248,8 @@ def train(run_fn, policy: str, n_steps: int, lengths_fn, gset=GAMMA_SET, P=PATIE
     out = []
     for t in range(n_steps):
         g = gamma if policy == "adaptive" else int(gset[0])
-        r = run_fn(policy, g, tau_at(tau_meas, gamma_meas, g), lengths_fn(t), t)
+        tau_prev = tau_at(tau_meas, gamma_meas, g) if tau_carry else tau_meas
+        r = run_fn(policy, g, tau_prev, lengths_fn(t), t)
         if r.tau is not None:
             tau_meas, gamma_meas = r.tau, g
             if policy == "adaptive":
@@ -286,6 +288,9 @@ def main(argv=None):
     ap.add_argument("--calib", default="", help="calibrate.py --out JSON; default: calibrate now on this model")
     ap.add_argument("--calib-B", default="1,4,16,64,128")
     ap.add_argument("--calib-S", default="512,2048,4096")
+    ap.add_argument("--tau-carry", action="store_true",
+                    help="carry the toggle's tau to a new draft length through the acceptance rate "
+                         "(default: Algorithm 1 as written, the measured tau as it is)")
     ap.add_argument("--out", default="")
     a = ap.parse_args(argv)
     log = lambda *x: print(*x, file=sys.stderr, flush=True)
@@ -308,7 +313,8 @@ def main(argv=None):
     ro.run("sd", GAMMA_SET[0], float(GAMMA_SET[0]), cost, EPS, np.minimum(lengths_fn(0), 64), 99, keep_trace=False)
     results = {}
     for pol in a.policies.split(","):
-        rs = train(lambda p, g, tp, L, t: ro.run(p, g, tp, cost, EPS, L, t)[0], pol, a.steps, lengths_fn)
+        rs = train(lambda p, g, tp, L, t: ro.run(p, g, tp, cost, EPS, L, t)[0], pol, a.steps, lengths_fn,
+                   tau_carry=a.tau_carry)
         results[pol] = rs
         for r in rs:
             log(f"{pol:9s} step {r.step}: gamma {r.gamma:2d}  tau_prev {r.tau_prev:5.2f}  tau "
@@ -316,7 +322,7 @@ def main(argv=None):
                 f"AR iters {r.ar_iters:5d}  SD iters {r.sd_iters:5d}  SD on at B={r.switch_B}  prep {r.prep_ms:.1f} ms")
     ro.close()
     L0 = lengths_fn(0)
-    summary = dict(model=cfg["name"], drafter=a.drafter, B=a.B, prompt=a.prompt,
+    summary = dict(model=cfg["name"], drafter=a.drafter, B=a.B, prompt=a.prompt, tau_carry=a.tau_carry,
                    lengths=dict(median=a.median, sigma=a.sigma, lo=a.lmin, hi=a.lmax, mean_step0=float(L0.mean()),
                                 max_step0=int(L0.max())),
                    calib=dict(F_eff=calib["F_eff"], params=calib["params"]),
@@ -325,7 +331,8 @@ def main(argv=None):
     if a.out:
         with open(a.out, "w") as fh:
             json.dump(summary, fh)
-    print(json.dumps(dict(model=summary["model"], drafter=a.drafter, B=a.B, makespan_s=summary["makespan_s"],
+    print(json.dumps(dict(model=summary["model"], drafter=a.drafter, B=a.B, tau_carry=a.tau_carry,
+                          makespan_s=summary["makespan_s"],
                           tau={p: [r.tau for r in rs] for p, rs in results.items()},
                           gamma={p: [r.gamma for r in rs] for p, rs in results.items()},
                           switch_B={p: [r.switch_B for r in rs] for p, rs in results.items()})))

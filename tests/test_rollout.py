@@ -146,13 +146,19 @@ def test_training_loop_feeds_tau_and_moves_gamma_with_patience():
     # two measured taus, 7.8 and 2.0, are both <= 1 + 9 * 0.85 = 8.65, which moves it back to 7
     assert [c[0] for c in calls] == [5, 5, 7, 7, 9, 9, 7]
     assert [r.gamma for r in rs] == [5, 5, 7, 7, 9, 9, 7]
-    # the toggle's tau: the last measured one, carried to the new draft length when gamma moved
+    # Algorithm 1 as written: the toggle gets the last measured tau as it is
+    assert [c[1] for c in calls] == [5.0, 5.8, 5.8, 7.8, 7.8, 7.8, 2.0]
+    # the carry variant: the last measured tau moved to the new draft length when gamma changed
+    run_fn3, calls3 = scripted_run(taus)
+    rollout.train(run_fn3, "adaptive", len(taus), lambda t: None, tau_carry=True)
+    assert [c[0] for c in calls3] == [5, 5, 7, 7, 9, 9, 7]
+
     def carried(tau, g0, g1):
         a = sdrl.alpha_from_tau(tau, g0)
         return sum(a ** i for i in range(g1 + 1))
     want = [5.0, 5.8, carried(5.8, 5, 7), 7.8, carried(7.8, 7, 9), carried(7.8, 7, 9), carried(2.0, 9, 7)]
-    assert [c[1] for c in calls] == pytest.approx(want, rel=1e-9)
-    assert calls[2][1] > 5.8 and calls[6][1] < 2.0
+    assert [c[1] for c in calls3] == pytest.approx(want, rel=1e-9)
+    assert calls3[2][1] > 5.8 and calls3[6][1] < 2.0
     run_fn2, calls2 = scripted_run(taus)
     rollout.train(run_fn2, "toggle", len(taus), lambda t: None)
     assert {c[0] for c in calls2} == {5}                         # fixed gamma_low without the adaptive policy
