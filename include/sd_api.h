@@ -215,6 +215,27 @@ sd_status sd_accept(sd_engine e, int32_t B, const int32_t* slots, const int32_t*
                     float temperature, sd_rng rng, int32_t* out_tok, int32_t* n_emit, int32_t* next_tok,
                     void* stream);
 
+/* The rejection sampler of sd_accept for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): no engine, and no hipMalloc, hipFree or
+ * allocating library call.  The same kernels as sd_accept, with the same
+ * decisions and outputs; the engine's state becomes arguments: vocab, and
+ * kv_len (device int32[max_slots]) holding each slot's cached length, which
+ * places the Philox counters exactly as in sd_accept (slots[b] must lie in
+ * [0, max_slots)).  All other arguments, layouts and outputs as sd_accept.
+ * Scratch: the kernels' partial results live in a static device array of
+ * 2^20 floats (4 MiB) per GPU, held until the process ends; a call needs
+ * B*(gamma+1)*C*2 + B*C*4 + 6*B + 4 floats with C = ceil(vocab / 4096)
+ * vocabulary chunks, and a larger one returns SD_E_INVAL before launching
+ * anything.  Every call on a GPU shares that GPU's array: calls whose work
+ * overlaps on one GPU (different streams, or threads) race and must not be
+ * made.  A slot index outside [0, max_slots) yields n_emit = 0, out_tok
+ * row -1 and next_tok -1 for that row (there is no engine to report it). */
+sd_status sd_accept_noalloc(int32_t B, int32_t vocab, const int32_t* slots, const int32_t* kv_len,
+                            int32_t max_slots, const int32_t* draft_tok, const float* q_logits,
+                            const float* q_stats, const float* p_logits, int32_t gamma, float temperature,
+                            sd_rng rng, int32_t* out_tok, int32_t* n_emit, int32_t* next_tok, void* stream);
+
 /* KV rollback (App. D.1): kv_len[slots[b]] += n_emit[b]; positions at or
  * beyond the new length (the rejected drafts' KV) are discarded.  With the
  * debug poison switch on, the discarded span is overwritten with NaN. */

@@ -6,6 +6,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <limits.h>
+
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -590,6 +593,67 @@ extern "C" sd_status sd_accept(sd_engine e, int32_t B, const int32_t* slots, con
     launch_accept(r, gamma, e->c.vocab, T, rg, draft_tok, q_logits, q_stats, p_logits, out_tok, n_emit, next_tok,
                   e->samp_part, e->acc_work, (hipStream_t)stream);
     return launched("sd_accept");
+}
+
+// ------------------------------------------------------- accept without allocating
+// sd_accept_noalloc's scratch: the rejection sampler's partial results
+// (launch_accept's part and work) and its device error words.  One copy per
+// GPU, held until the process ends; every call on a GPU shares it, and
+// nothing in it has to start at zero (each call writes every partial it later
+// reads).  In host code `scratch` names a host-side stand-in: kernels get the
+// per-device address from hipGetSymbolAddress instead.
+constexpr size_t NOALLOC_FLOATS = (size_t)1 << 20;      // 4 MiB
+static __device__ __align__(256) float scratch[NOALLOC_FLOATS];
+
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static float* g_scratch_dev[NOALLOC_MAX_DEVICES];
+static std::once_flag g_scratch_once[NOALLOC_MAX_DEVICES];
+static hipError_t g_scratch_status[NOALLOC_MAX_DEVICES];
+
+// The current device's copy of `scratch`, looked up once per device with that
+// device current.
+static sd_status noalloc_scratch(float** out)
+{
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= NOALLOC_MAX_DEVICES)
+        return fail(SD_E_UNSUPPORTED, "device %d beyond the %d this library tracks", dev, NOALLOC_MAX_DEVICES);
+    std::call_once(g_scratch_once[dev], [dev] {
+        void* p = nullptr;
+        g_scratch_status[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_dev[dev] = (float*)p;
+    });
+    if (g_scratch_status[dev] != hipSuccess || !g_scratch_dev[dev])
+        return fail(SD_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                    hipGetErrorString(g_scratch_status[dev]));
+    *out = g_scratch_dev[dev];
+    return SD_OK;
+}
+
+extern "C" sd_status sd_accept_noalloc(int32_t B, int32_t vocab, const int32_t* slots, const int32_t* kv_len,
+                                       int32_t max_slots, const int32_t* draft_tok, const float* q_logits,
+                                       const float* q_stats, const float* p_logits, int32_t gamma, float T,
+                                       sd_rng rng, int32_t* out_tok, int32_t* n_emit, int32_t* next_tok,
+                                       void* stream)
+{
+    if (!slots || !kv_len || !draft_tok || !q_logits || !q_stats || !p_logits || !out_tok || !n_emit)
+        return fail(SD_E_INVAL, "NULL buffer");
+    if (B < 1 || vocab < 1 || max_slots < 1) return fail(SD_E_INVAL, "need B, vocab, max_slots >= 1");
+    if (gamma < 1 || gamma > 64) return fail(SD_E_INVAL, "gamma=%d outside [1, 64]", gamma);
+    if (!(T > 0.f) || !isfinite(T)) return fail(SD_E_INVAL, "temperature must be finite and > 0");
+    const size_t part = accept_part_floats(B, gamma, vocab), work = accept_work_floats(B, gamma);
+    const size_t need = part + work + ERR_COUNT;
+    if (need > NOALLOC_FLOATS)
+        return fail(SD_E_INVAL, "B=%d, gamma=%d, vocab=%d need %zu scratch floats, the maximum is %zu", B, gamma,
+                    vocab, need, NOALLOC_FLOATS);
+    float* sc = nullptr;
+    sd_status st = noalloc_scratch(&sc);
+    if (st != SD_OK) return st;
+    rows_t r = {B, 1, 0, slots, kv_len, max_slots, INT_MAX, (uint32_t*)(sc + part + work)};
+    rng_t rg = {rng.seed, rng.step};
+    launch_accept(r, gamma, vocab, T, rg, draft_tok, q_logits, q_stats, p_logits, out_tok, n_emit, next_tok, sc,
+                  sc + part, (hipStream_t)stream);
+    return launched("sd_accept_noalloc");
 }
 
 extern "C" sd_status kv_rollback(sd_engine e, int32_t B, const int32_t* slots, const int32_t* n_emit, void* stream)

@@ -136,3 +136,4 @@ void launch_accept(const rows_t& r, int gamma, int V, float T, rng_t rng, const 
                    int32_t* out_tok, int32_t* n_emit, int32_t* next_tok, float* part,
                    float* work, hipStream_t s);
 size_t accept_work_floats(int B, int gamma);
+size_t accept_part_floats(int B, int gamma, int V);

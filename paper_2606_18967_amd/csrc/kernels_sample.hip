@@ -434,6 +434,14 @@ size_t sample_part_floats(int rows, int V) { return (size_t)rows * sample_chunks
 
 size_t accept_work_floats(int B, int gamma) { (void)gamma; return (size_t)B * WK; }
 
+// launch_accept's part: (max, sumexp) per (p row, chunk), then the final
+// draw's (keyA, idxA, keyB, idxB) per (sequence, chunk)
+size_t accept_part_floats(int B, int gamma, int V)
+{
+    const size_t nch = (size_t)sample_chunks(V);
+    return (size_t)B * (gamma + 1) * nch * 2 + (size_t)B * nch * 4;
+}
+
 void launch_sample(const rows_t& r, const float* logits, long ld, int V, float T, rng_t rng, int pos_off,
                    int32_t* tok, int tok_stride, float* stats, int stats_stride, float* part, hipStream_t s)
 {

@@ -31,7 +31,7 @@ API_SYMBOLS = (
     "sd_prefill", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
-    "sd_alpha_from_tau", "sd_timing", "sd_timing_read", "sd_dense_gemm_bf16",
+    "sd_alpha_from_tau", "sd_timing", "sd_timing_read", "sd_dense_gemm_bf16", "sd_accept_noalloc",
 )
 
 # kernel classes of sd_timing_read
@@ -99,6 +99,7 @@ def lib():
             "sd_draft": (_i32, [_P, _i32, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
             "sd_verify": (_i32, [_P, _i32, _P, _P, _P, _i32, _P, _P]),
             "sd_accept": (_i32, [_P, _i32, _P, _P, _P, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
+            "sd_accept_noalloc": (_i32, [_i32, _i32, _P, _P, _i32, _P, _P, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
             "kv_rollback": (_i32, [_P, _i32, _P, _P, _P]),
             "sd_ar_step": (_i32, [_P, _i32, _P, _P, _f, Rng, _P, _P, _P]),
             "sd_sync": (_i32, [_P, _P]),
@@ -372,6 +373,27 @@ class StepGraph:
 
     def replay(self):
         self.graph.replay()
+
+
+def accept_noalloc(slots, kv_len, draft_tok, q_logits, q_stats, p_logits, gamma, T, seed, step, out_tok, n_emit,
+                   next_tok=None):
+    """sd_accept_noalloc: the rejection sampler with no engine and no device
+    allocation (its scratch is the library's static per-GPU array).  kv_len
+    is the caller's int32 [max_slots] cache-length array; the other buffers
+    as Engine.accept."""
+    B = slots.numel()
+    V = q_logits.shape[-1]
+    dev = slots.device
+    nt = _dev(next_tok, "next_tok", torch.int32, (B,), dev) if next_tok is not None else None
+    _check(lib().sd_accept_noalloc(B, V, _dev(slots, "slots", torch.int32, (B,), dev),
+                                   _dev(kv_len, "kv_len", torch.int32, None, dev), kv_len.numel(),
+                                   _dev(draft_tok, "draft_tok", torch.int32, (B, gamma), dev),
+                                   _dev(q_logits, "q_logits", torch.float32, (B, gamma, V), dev),
+                                   _dev(q_stats, "q_stats", torch.float32, (B, gamma, 2), dev),
+                                   _dev(p_logits, "p_logits", torch.float32, (B, gamma + 1, V), dev),
+                                   gamma, T, Rng(seed, step),
+                                   _dev(out_tok, "out_tok", torch.int32, (B, gamma + 1), dev),
+                                   _dev(n_emit, "n_emit", torch.int32, (B,), dev), nt, _stream()))
 
 
 def dense_gemm_bf16(A: torch.Tensor, W: torch.Tensor, out: torch.Tensor):
