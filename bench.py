@@ -1,19 +1,21 @@
 #!/usr/bin/env python3
 """Throughput of the quantized self-speculative decoding step on one MI355X.
 
-Workload: the 8B-shaped decoder (4 layers, hidden 4096, 32 query / 8 KV heads
-x 128, SwiGLU FFN 14336, vocab 128256, bf16, random init), int4 group-128
-drafter refreshed from it (or, with --drafter, its asymmetric-int4 or int8
-variant), B = 64 sequences with 2048 positions of random
-bf16 KV context each, gamma = 4, temperature 1.0.  One step = gamma draft
-forwards + one verify forward over B*(gamma+1) positions + accept + KV
-rollback + the host read of n_emit.  The metric is accepted (emitted)
-tokens per second.
+Default workload: the 64-layer 32B-shaped decoder (hidden 5120, 40 query / 8
+KV heads x 128, SwiGLU FFN 27648, vocab 152064, bf16, random init) with the
+int4 group-128 drafter refreshed from it, B = 64 sequences with 8192
+positions of random bf16 KV context each, gamma = 4, temperature 1.0 (the
+largest shape that fits one GPU: B = 128 at 8192 positions needs ~360 GB).
+--model L4_8B runs the 4-layer 8B-shaped stack at B = 64 and 2048 positions.
+One step = gamma draft forwards + one verify forward over B*(gamma+1)
+positions + accept + KV rollback + the host read of n_emit.  The metric is
+accepted (emitted) tokens per second.
 
 The JSON line also carries: the GPU's own AR decode rate at the same batch,
 per-kernel-class times measured with HIP events on the launch stream, the
 roofline record of the dominant kernel class, and the CPU oracle timed on
-the host on a bounded sample of the same workload.
+the host on a bounded sample of the same workload and extrapolated over the
+layers.
 """
 from __future__ import annotations
 
@@ -37,7 +39,6 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--ar-steps", type=int, default=20)
-    ap.add_argument("--cpu-seqs", type=int, default=12, help="sequences in the oracle's CPU sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--drafter", choices=("w4", "w4a", "w8"), default="w4",
                     help="drafter format: RTN int4 symmetric (default), int4 asymmetric, int8")
@@ -45,12 +46,12 @@ def parse():
                     help="bind a paged KV cache with pages of this many positions, shuffled (0: dense cache)")
     ap.add_argument("--graph", action="store_true",
                     help="time the SD steps as replays of one captured HIP graph")
-    ap.add_argument("--batch", type=int, default=0, help="sequences (default: the 64 of the workload)")
-    ap.add_argument("--context", type=int, default=0, help="cached positions per sequence (default 2048)")
+    ap.add_argument("--batch", type=int, default=0, help="sequences (default: the workload's)")
+    ap.add_argument("--context", type=int, default=0, help="cached positions per sequence (default: the workload's)")
     ap.add_argument("--gamma", type=int, default=0, help="draft length (default 4)")
-    ap.add_argument("--model", choices=("L4_8B", "L32_8B", "L64_32B"), default="L4_8B",
-                    help="decoder: the 8B shape with 4 layers (the default workload) or 32, or the 32B shape "
-                         "with 64 layers (no CPU-oracle leg for the two large ones)")
+    ap.add_argument("--model", choices=("L64_32B", "L4_8B", "L32_8B"), default="L64_32B",
+                    help="decoder: the 32B shape with 64 layers (the default workload: B = 64, 8192 positions), "
+                         "or the 8B shape with 4 or 32 layers (B = 64, 2048 positions)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -84,13 +85,16 @@ def kernel_sources_hash(files=None):
     return h.hexdigest()[:16]
 
 
-# the workload the committed counter runs time (bench.py's defaults)
-DEFAULT_WORKLOAD = "L4_8B B=64 S=2048 gamma=4 w4 page=0"
-
-
 def workload_key(model, B, S, gamma, drafter, page):
     return f"{model} B={B} S={S} gamma={gamma} {drafter} page={page}"
 
+
+# the workload the committed counter runs time (bench.py's defaults)
+DEFAULT_WORKLOAD = workload_key("L64_32B", 64, 8192, 4, "w4", 0)
+METRIC = "accepted tokens/s per GPU per SD step; draft/verify HBM GB/s & MFMA % of peak"
+RUNS = {"L4_8B": "L4_8B_RUN", "L32_8B": "L32_8B_RUN", "L64_32B": "L64_32B_RUN"}
+WORKLOAD_NAMES = {"L4_8B": "8B-shaped decoder, 4 layers", "L32_8B": "8B-shaped decoder, 32 layers",
+                  "L64_32B": "32B-shaped decoder, 64 layers"}
 
 def measured_traffic(kind: str, workload: str = DEFAULT_WORKLOAD):
     """HBM bytes per launch from committed rocprofv3 counter runs, or None if
@@ -242,7 +246,7 @@ def main():
 
     from paper_2606_18967_amd import sdrl, synth
 
-    cfg, run = getattr(synth, args.model), synth.L4_8B_RUN
+    cfg, run = getattr(synth, args.model), getattr(synth, RUNS[args.model])
     B, S, gamma, T, seed = run["B"], run["context"], run["gamma"], run["T"], run["seed"]
     B, S, gamma = args.batch or B, args.context or S, args.gamma or gamma
     n_steps, n_warm = args.steps, args.warmup
@@ -289,6 +293,7 @@ def main():
     bufs = sdrl.SDBuffers(eng, B, gamma)
     tok = [synth.make_tokens(B, 1, cfg["vocab"], seed + 7)[:, 0].to(dev).contiguous(),
            torch.zeros(B, dtype=torch.int32, device=dev)]
+    first_tok = int(tok[0][0].item())
     state = dict(it=0, emitted=0)
 
     def sd_iter():
@@ -397,11 +402,11 @@ def main():
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
-    if not args.no_cpu_baseline and not args.page_size and args.model == "L4_8B":
-        cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, args.drafter)
+    if not args.no_cpu_baseline and not args.page_size:
+        cpu = cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, args.drafter, tau, first_tok)
 
     rec = {
-        "metric": "accepted tokens/s per GPU per SD step",
+        "metric": METRIC,
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -413,8 +418,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": {"L4_8B": "8B-shaped decoder, 4 layers", "L32_8B": "8B-shaped decoder, 32 layers",
-                                "L64_32B": "32B-shaped decoder, 64 layers"}[args.model] + ", bf16 target + "
+        "config": {"workload": WORKLOAD_NAMES[args.model] + ", bf16 target + "
                                + {"w4": "int4 g128", "w4a": "asymmetric int4 g128", "w8": "int8 g128"}[args.drafter]
                                + f" drafter, B={B}, KV context {S} (random N(0,1)), gamma={gamma}, T=1.0",
                    "drafter": args.drafter, "hip_graph": bool(args.graph), "kv_page_size": args.page_size,
@@ -435,36 +439,90 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, fmt="w4"):
-    """The oracle (plain C, OpenMP over projection rows) on the host: one SD
-    step for the first `cpu_seqs` sequences of the workload, from the same
-    weights and KV context."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(args, cfg, W, k, v, S, gamma, T, seed, fmt, tau_gpu, tok):
+    """The oracle (plain C, fp64 model arithmetic, OpenMP over projection
+    rows) on the host, on a bounded sample of the same workload, extrapolated
+    over the layers.
+
+    All cores: one SD step of sequence 0 (gamma drafter forwards, the verify
+    forward over gamma + 1 tokens, the accept) with the workload's first one
+    and first two layers (same embedding, final norm and LM head, same KV
+    context): T(L) = T(1) + (L - 1) (T(2) - T(1)).  One core: the drafter's
+    and the target's one-token forwards at one and two layers, extrapolated
+    the same way and composed into gamma drafter + (gamma + 1) target token
+    forwards.  The value is the GPU's measured tokens per sequence per step
+    over T(L): the oracle's throughput on the full model, by extrapolation."""
     import numpy as np
 
     import oracle
     from paper_2606_18967_amd import synth
 
-    log(args, "cpu baseline: copying weights to host ...")
-    Wh = [synth.to_numpy_bits(w) for w in W]
-    target = oracle.Model(cfg, Wh, oracle.BF16)
-    drafter = oracle.make_drafter(cfg, Wh, oracle.BF16, fmt=fmt)
+    L = cfg["n_layers"]
+    log(args, "cpu baseline: host copies of the first two layers ...")
+    idx = list(range(3)) + list(range(3, 15))
+    Wh = [synth.to_numpy_bits(W[i]) for i in idx]
+    models = {}
+    for nl in (1, 2):
+        c = dict(cfg, n_layers=nl)
+        t = oracle.Model(c, Wh[:3 + 6 * nl], oracle.BF16)
+        d = oracle.make_drafter(c, Wh[:3 + 6 * nl], oracle.BF16, fmt=fmt)
+        models[nl] = (c, t, d)
     cap = S + gamma + 2
-    toks = synth.make_tokens(64, 1, cfg["vocab"], seed + 7)[:, 0].numpy()   # the workload's first tokens
-    emitted, elapsed = 0, 0.0
-    for b in range(args.cpu_seqs):
-        kvb = oracle.KV(cfg, cap)
-        kvb.k[:, :, :S] = k[:, b, :, :S].float().cpu().numpy()
-        kvb.v[:, :, :S] = v[:, b, :, :S].float().cpu().numpy()
+    kk = k[:2, 0, :, :S].float().cpu().numpy()
+    vv = v[:2, 0, :, :S].float().cpu().numpy()
+
+    def fresh_kv(nl):
+        kv = oracle.KV(models[nl][0], cap)
+        kv.k[:, :, :S], kv.v[:, :, :S] = kk[:nl], vv[:nl]
+        return kv
+
+    oracle.set_threads(0)
+    cores = oracle.get_threads()
+    t_all = {}
+    for nl in (1, 2):
+        kv = fresh_kv(nl)
         t0 = time.perf_counter()
-        r = oracle.sd_step_seq(target, drafter, kvb, S, int(toks[b]), gamma, T, seed, 1, b)
-        elapsed += time.perf_counter() - t0
-        emitted += r["n_emit"]
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    log(args, f"cpu baseline: {emitted} tokens in {elapsed:.2f}s")
-    return dict(value=round(emitted / elapsed, 3), unit="tokens/s", cores=threads, kind="oracle",
-                sample=f"one SD step (gamma={gamma}: {gamma} draft + {gamma + 1} verify token forwards, "
-                       f"accept) for {args.cpu_seqs} of the 64 sequences, same weights and KV context",
-                seconds=round(elapsed, 2), tokens=emitted)
+        oracle.sd_step_seq(models[nl][1], models[nl][2], kv, S, tok, gamma, T, seed, 1, 0)
+        t_all[nl] = time.perf_counter() - t0
+    step_all = t_all[1] + (L - 1) * (t_all[2] - t_all[1])
+    oracle.set_threads(1)
+    t_one = {}
+    try:
+        for nl in (1, 2):
+            for which, m in (("draft", models[nl][2]), ("target", models[nl][1])):
+                kv = fresh_kv(nl)
+                t0 = time.perf_counter()
+                oracle.forward_seq(m, kv, [tok], S)
+                t_one[(which, nl)] = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(0)
+    ext = lambda w: t_one[(w, 1)] + (L - 1) * (t_one[(w, 2)] - t_one[(w, 1)])
+    step_one = gamma * ext("draft") + (gamma + 1) * ext("target")
+    sample_s = sum(t_all.values()) + sum(t_one.values())
+    log(args, f"cpu baseline: {step_all:.1f} s per SD step per sequence on {cores} cores, {step_one:.1f} s on one, "
+              f"by extrapolation to {L} layers ({sample_s:.1f} s measured)")
+    return dict(value=round(tau_gpu / step_all, 5), unit="tokens/s", cores=cores, kind="oracle",
+                sample=(f"extrapolation over the layers: one SD step (gamma={gamma}: {gamma} drafter forwards, a "
+                        f"{gamma + 1}-token verify forward, accept) of one sequence with the workload's first 1 "
+                        f"and 2 layers (same embedding, LM head and {S}-position KV context), "
+                        f"T(L) = T(1) + (L-1)(T(2)-T(1)) at L={L}; tokens per step = the GPU's measured tau"),
+                extrapolated=True, seconds_per_step=round(step_all, 3), measured_seconds=round(sample_s, 2),
+                single_thread=dict(value=round(tau_gpu / step_one, 6), seconds_per_step=round(step_one, 3),
+                                   sample="one-token drafter and target forwards at 1 and 2 layers, extrapolated "
+                                          f"to {L} layers, composed into {gamma} drafter + {gamma + 1} target "
+                                          "token forwards"),
+                cpu_model=_cpu_model(), nproc=os.cpu_count())
 
 
 if __name__ == "__main__":

@@ -98,6 +98,8 @@ def _declare(L):
         "or_decode_breakdown": (None, [_i, _i, _i, _i, _i, _i, _i, _d, _d, _d, _d, _d, _d, _P]),
         "or_sample_hist": (None, [_P, _i, _f, _u64, _u64, _i, _P]),
         "or_accept_hist": (None, [_P, _P, _i, _f, _u64, _u64, _i, _P, _P]),
+        "or_set_threads": (None, [_i]),
+        "or_get_threads": (_i, []),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -111,6 +113,15 @@ def _ptr(a: np.ndarray | None):
         return None
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data_as(C.c_void_p)
+
+
+def set_threads(n: int = 0):
+    """Threads of the oracle's parallel loops (n <= 0: every host core)."""
+    lib().or_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().or_get_threads())
 
 
 # ---------------------------------------------------------------- scalars

@@ -20,6 +20,7 @@
  * for RL Rollouts".  Sections are cited by number and label.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -833,3 +834,14 @@ OR_API void or_accept_hist(const float* q, const float* p12, int V, float T, uin
         if (ne == 2) (*n_acc)++;
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Threads of the parallel loops (timing of the oracle on one or all host    */
+/* cores); n <= 0 restores every core.                                       */
+/* ------------------------------------------------------------------------ */
+OR_API void or_set_threads(int n)
+{
+    omp_set_num_threads(n > 0 ? n : omp_get_num_procs());
+}
+
+OR_API int or_get_threads(void) { return omp_get_max_threads(); }

@@ -28,6 +28,10 @@ L64_32B = dict(name="32B-shape-64L", n_layers=64, hidden=5120, n_q=40, n_kv=8, h
 # Workloads (batch, context, draft length, temperature).
 TINY_RUN = dict(B=4, prompt=64, context=128, gamma=4, T=1.0, seed=0)
 L4_8B_RUN = dict(B=64, context=2048, gamma=4, T=1.0, seed=1)
+L32_8B_RUN = dict(B=64, context=2048, gamma=4, T=1.0, seed=2)
+# the 64-layer 32B shape at B = 128 and 8192 positions needs ~360 GB; one GPU
+# holds it at B = 64 and 8192 positions (~224 GB with weights and drafter)
+L64_32B_RUN = dict(B=64, context=8192, gamma=4, T=1.0, seed=5)
 
 
 def weight_shapes(cfg: dict):
