@@ -191,15 +191,21 @@ def test_dense_gemm_wide_dma_tiles(M):
     assert err <= 1e-4 * ref.abs().max().item(), err
 
 
+# FFN wide enough (24576) that the drafter's gate/up projection runs without a
+# K split, which is where its SwiGLU epilogue is used
+WIDE_FFN = dict(name="wide-ffn-bf16", n_layers=1, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=24576, vocab=256,
+                dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
+
+
 @pytest.mark.parametrize("fmt", ["w4", "w4a", "w8"])
-@pytest.mark.parametrize("B", [3, 16, 64])
-def test_fused_swiglu_equals_separate_kernel(B, fmt):
-    """SwiGLU in the gate/up GEMM's epilogue (int4 drafter GEMM with one or two
-    32-row tiles; the tiled bf16 verify GEMM at 80 and 320 rows) gives the
-    same SD step, bit for bit, as the gate/up GEMM followed by the SwiGLU
-    kernel: same fp32 sums, same SiLU."""
-    say("fused swiglu", B, fmt)
-    cfg = SMALL_BF16
+@pytest.mark.parametrize("B,cfg", [(3, SMALL_BF16), (16, SMALL_BF16), (64, SMALL_BF16), (20, WIDE_FFN),
+                                   (64, WIDE_FFN)], ids=["3", "16", "64", "wide-20", "wide-64"])
+def test_fused_swiglu_equals_separate_kernel(B, cfg, fmt):
+    """SwiGLU in the gate/up GEMM's epilogue (the int4 drafter GEMM with one or
+    two 32-row tiles where it runs unsplit; the tiled bf16 verify GEMM at 80
+    and 320 rows) gives the same SD step, bit for bit, as the gate/up GEMM
+    followed by the SwiGLU kernel: same fp32 sums, same SiLU."""
+    say("fused swiglu", B, cfg["name"], fmt)
     gamma, T, seed, S = 4, 1.0, 31, 48
     W = [w.cuda() for w in synth.make_weights(cfg, 13, "cpu")]
     eng, k, v, kv_len = make_engine(cfg, W, B, S + gamma + 4, gamma, fmt=fmt)
