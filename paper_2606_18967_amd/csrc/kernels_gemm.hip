@@ -487,8 +487,8 @@ __global__ void __launch_bounds__(256) k_gemm_t32(const uint16_t* __restrict__ A
 // bank conflicts; a DMA lane therefore fetches chunk pos ^ sw(r) of its row.
 // WN = 2: 320 x 128 tiles, 4 waves; WN = 4: 320 x 256 tiles, 8 waves (half the
 // activation re-reads per weight byte, for launches with a full wave of tiles).
-// SW: the SwiGLU epilogue; the tile takes 64 features, and wave column wn's
-// two 32-column blocks are the gate rows and the up rows of the same 32
+// SW: the SwiGLU epilogue; the tile takes 32 WN features, and wave column
+// wn's two 32-column blocks are the gate rows and the up rows of the same 32
 // features, so SiLU(g) u is formed in registers (no split-K there).  With S
 // K splits the partial sums go to P[s][M][N] as in k_gemm_t32.
 constexpr int DBK = 64, DRB = DBK * 2;                  // k per stage, bytes per tile row
@@ -519,7 +519,7 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
     constexpr int STG = (BM + BN) * DRB;
     constexpr int CNT = NI / NWAVE;                            // pieces per wave per stage
     static_assert(NI % NWAVE == 0, "every wave issues the same number of pieces");
-    static_assert(!SW || WN == 2, "the SwiGLU form uses 64-feature tiles");
+    constexpr int FT = 32 * WN;                                // features per tile of the SwiGLU form
     __shared__ __attribute__((aligned(1024))) uint8_t sm[2 * STG];
     const uint32_t sbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sm;
     const int per_xcd = gridDim.x >> 3;
@@ -547,7 +547,7 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
             const int row = 8 * (t - NA) + rl;
             int wrow = n0 + row;
             if constexpr (SW) {
-                const int f = nt * 64 + (row >> 6) * 32 + (row & 31);   // wave column row/64, block (row/32)%2
+                const int f = nt * FT + (row >> 6) * 32 + (row & 31);   // wave column row/64, block (row/32)%2
                 wrow = ((row >> 5) & 1) ? N / 2 + f : f;
             }
             src[q] = W + (size_t)wrow * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
@@ -598,7 +598,7 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
         }
     }
     if constexpr (SW) {
-        const int F = N / 2, feat = nt * 64 + wn * 32 + (lane & 31);
+        const int F = N / 2, feat = nt * FT + wn * 32 + (lane & 31);
 #pragma unroll
         for (int i = 0; i < MTW / 2; ++i)
 #pragma unroll
@@ -747,6 +747,36 @@ static void tiled_plan(int M, int N, int K, int* mtw, int* S)
     *S = s;
 }
 
+// 320-row tiles: without a K split where 320 x 256 tiles (eight waves, half
+// the activation bytes per weight byte of 320 x 128) or else 320 x 128 tiles
+// give DMA_SPLIT_TARGET work-groups; otherwise 320 x 256 tiles (where N
+// allows) and the smallest split S of the K / 64 stages (at least two per
+// split, at most DMA_MAX_SPLIT) that gives that many.  The register-staged
+// tiles and the SwiGLU form take the same S, so every form sums the same
+// products in the same order.
+#ifndef DMA_SPLIT_TARGET
+#define DMA_SPLIT_TARGET 192
+#endif
+#ifndef DMA_MAX_SPLIT
+#define DMA_MAX_SPLIT 32
+#endif
+
+static void dma_plan(int M, int N, int K, int* wn, int* S)
+{
+    const int mtiles = (M + 319) / 320;
+    *S = 1;
+    if (N % 256 == 0 && N / 256 * mtiles >= DMA_SPLIT_TARGET) { *wn = 4; return; }
+    if (N / 128 * mtiles >= DMA_SPLIT_TARGET) { *wn = 2; return; }
+    *wn = N % 256 == 0 ? 4 : 2;
+    const int tiles = N / (64 * *wn) * mtiles;
+    const int KB = K / 64;
+    for (int s = 1; s <= DMA_MAX_SPLIT && 2 * s <= KB; ++s) {
+        if (KB % s) continue;
+        *S = s;
+        if (tiles * s >= DMA_SPLIT_TARGET) break;
+    }
+}
+
 size_t gemm_part_floats(int M, int N, int K)
 {
     int nbw, S;
@@ -754,6 +784,10 @@ size_t gemm_part_floats(int M, int N, int K)
     if (use_tiled(M, N, K)) {
         int mtw, St;
         tiled_plan(M, N, K, &mtw, &St);
+        if (mtw == 10) {
+            int wn;
+            dma_plan(M, N, K, &wn, &St);
+        }
         S = St > S ? St : S;
     }
     return S > 1 ? (size_t)S * M * N : 0;
@@ -776,18 +810,17 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
                      int ldc, gemm_mode mode, bool defer_reduce, hipStream_t s, bool lds_dma)
 {
     if (use_tiled(M, N, K)) {
-        int mtw, S;
+        int mtw, S, wn = 2;
         tiled_plan(M, N, K, &mtw, &S);
+        if (mtw == 10) dma_plan(M, N, K, &wn, &S);
         if (S > 1 && (size_t)S * M * N > part_cap) S = 1;
         int mtiles = (M + 32 * mtw - 1) / (32 * mtw);
         if (lds_dma && mtw == 10) {
-            // 320-row tiles: the DMA-fed kernel, 256 columns per tile when
-            // that still gives a full wave of work-groups without split-K
-            const bool wide = S == 1 && N % 256 == 0 && N / 256 * mtiles >= 256;
-            const int total = N / (wide ? 256 : 128) * mtiles * S;
+            // 320-row tiles: the DMA-fed kernel
+            const int total = N / (64 * wn) * mtiles * S;
             dim3 grid((total + 7) / 8 * 8);
-            if (wide)
-                k_gemm_dma<4, false><<<grid, 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, 1, mtiles, total, nullptr, 0);
+            if (wn == 4)
+                k_gemm_dma<4, false><<<grid, 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0);
             else
                 k_gemm_dma<2, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0);
             if (S > 1 && !defer_reduce) {
@@ -843,9 +876,21 @@ int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act
     const int total = F / 64 * mtiles;
     dim3 grid((total + 7) / 8 * 8);
     const int N = 2 * F;
-    if (lds_dma && mtw == 10) {
-        k_gemm_dma<2, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t);
-        return 1;
+    if (mtw == 10) {
+        // fused only where the plain projection would run unsplit (the same
+        // products summed in the same order either way)
+        int wn, S;
+        dma_plan(M, N, K, &wn, &S);
+        if (S != 1) return 0;
+        if (lds_dma) {
+            const int tot = F / (32 * wn) * mtiles;
+            dim3 g((tot + 7) / 8 * 8);
+            if (wn == 4)
+                k_gemm_dma<4, true><<<g, 512, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, tot, out, out_t);
+            else
+                k_gemm_dma<2, true><<<g, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, tot, out, out_t);
+            return 1;
+        }
     }
     switch (mtw) {
         case 10: k_gemm_t32<10, true><<<grid, 256, 0, s>>>(A, W, nullptr, nullptr, M, N, K, 0, 0, 1, mtiles, total, out, out_t); break;
