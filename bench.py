@@ -113,14 +113,19 @@ def measured_traffic(kind: str, workload: str = DEFAULT_WORKLOAD):
     return d.get("bytes")
 
 
-# the kernel each timing class brackets (bf16 KV cache, head_dim 128, M = 64 drafter rows)
+# the kernel each timing class brackets (bf16 KV cache, head_dim 128, M = 64 drafter rows, 320 verify rows)
 KERNEL_OF_CLASS = {
     "attn_decode": "k_attn_mfma<128, 1, false>",
     "attn_verify": "k_attn_mfma<128, 2, false>",
-    "int4_proj": "k_gemm_q4<2, 4, 0, false> (qkv, down; gate/up runs as the SwiGLU variant <2, 4, 0, true>)",
-    "bf16_proj": "k_gemm_dma<2, false> (qkv, o, down; gate/up runs as the SwiGLU variant <2, true>)",
+    "int4_proj": "k_gemm_q4<2, 0, false> (qkv, o, down; gate/up runs unsplit as the SwiGLU variant <2, 0, true> "
+                 "where N allows)",
+    "bf16_proj": "k_gemm_dma<4, false> (qkv, o, down; gate/up runs as the SwiGLU variant <4, true> where N allows)",
     "lm_head": "k_gemm_stream<2, 4, 8> (draft rows), k_gemm_dma<4, false> (verify rows)",
 }
+# the counter ingest keeps, per class, only the dispatches of its kernel
+# launched by that class (work-group counts tell the verify LM head, 594
+# 320x256 tiles at V = 152064, from the split projections, <= 240)
+CLASS_WG_FILTER = {"bf16_proj": lambda wgs: wgs < 500, "lm_head": lambda wgs: wgs >= 500}
 
 
 # bytes per quantized weight: codes + fp16 scale (+ zero point) per group of 128
@@ -206,18 +211,20 @@ def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, out_path):
 
     ff, fname, fkib = copy_factor(copy_fetch_csv, "FETCH_SIZE")
     wf, wname, wkib = copy_factor(copy_write_csv, "WRITE_SIZE")
-    # the projections' class keeps its own launches of the 128-column DMA
-    # kernel (<= 512 work-groups at 320 rows)
-    keep = {"k_gemm_dma<2,false>": lambda wgs: wgs <= 512}
-    fetch = per_kernel(fetch_csv, "FETCH_SIZE", keep)
-    write = per_kernel(write_csv, "WRITE_SIZE", keep)
+    fetch = {c: per_kernel(fetch_csv, "FETCH_SIZE", {kernel_key(KERNEL_OF_CLASS[c]): f})
+             for c, f in CLASS_WG_FILTER.items()}
+    write = {c: per_kernel(write_csv, "WRITE_SIZE", {kernel_key(KERNEL_OF_CLASS[c]): f})
+             for c, f in CLASS_WG_FILTER.items()}
+    fetch_all = per_kernel(fetch_csv, "FETCH_SIZE")
+    write_all = per_kernel(write_csv, "WRITE_SIZE")
     per = {}
     for cls, kname in KERNEL_OF_CLASS.items():
         k = kernel_key(kname)
-        if k not in fetch or k not in write:
+        fe, wr = (fetch[cls], write[cls]) if cls in CLASS_WG_FILTER else (fetch_all, write_all)
+        if k not in fe or k not in wr:
             continue
-        per[cls] = dict(kernel=k, fetch_bytes=fetch[k][0] * 1024 * ff, write_bytes=write[k][0] * 1024 * wf,
-                        bytes=fetch[k][0] * 1024 * ff + write[k][0] * 1024 * wf, dispatches=fetch[k][1],
+        per[cls] = dict(kernel=k, fetch_bytes=fe[k][0] * 1024 * ff, write_bytes=wr[k][0] * 1024 * wf,
+                        bytes=fe[k][0] * 1024 * ff + wr[k][0] * 1024 * wf, dispatches=fe[k][1],
                         sources=kernel_sources_hash(SOURCES_OF_CLASS[cls]))
     rec = {
            "workload": DEFAULT_WORKLOAD,
