@@ -128,7 +128,7 @@ __global__ void __launch_bounds__(64 * NW) k_gemm_stream(const uint16_t* __restr
         for (int i = 0; i < NBW; ++i) {
             const uint16_t* wp = Wt + (size_t)((nb0 + i) * 16 + (lane & 15)) * K + (size_t)phys(g) * SK + 8 * (lane >> 4);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) wq[i][j] = *(const u32x4*)(wp + 32 * j);
+            for (int j = 0; j < 4; ++j) wq[i][j] = *(const u32x4*)(wp + 32 * j);   // j, j + 1 share a 128-byte line: cached
         }
     };
 
@@ -498,6 +498,12 @@ __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_byte)
     asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(src), "{m0}"(lds_byte) : "memory");
 }
 
+// the same for data read once (weights): non-temporal
+__device__ __forceinline__ void lds_dma16_nt(const void* src, uint32_t lds_byte)
+{
+    asm volatile("global_load_lds_dwordx4 %0, off nt" : : "v"(src), "{m0}"(lds_byte) : "memory");
+}
+
 // s_waitcnt vmcnt(N) with the other counters left free (gfx9 field layout)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
@@ -556,7 +562,10 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
     }
     auto issue = [&](int buf, int kb) {
 #pragma unroll
-        for (int q = 0; q < CNT; ++q) lds_dma16(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+        for (int q = 0; q < CNT; ++q) {
+            if (wv + q * NWAVE < NA) lds_dma16(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+            else lds_dma16_nt(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+        }
     };
 
     floatx16 acc[MTW / 2][2];

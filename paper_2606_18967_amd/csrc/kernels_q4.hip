@@ -37,7 +37,8 @@
 // of a D-stage ring, and read back as MFMA A fragments; 16-byte chunk c of
 // row r sits at position c ^ (r & 15), so the fragment reads (16 rows at one
 // chunk per phase) are free of bank conflicts.  Each wave streams its own
-// weights from HBM into a ring of D register sets.  Group g + D - 1 is
+// weights from HBM (non-temporal loads: each weight is read once) into a
+// ring of D register sets.  Group g + D - 1 is
 // requested right after the barrier that opens group g.  Inside a group the
 // A fragments and dequantized weights of k-step s + 1 are formed while the
 // MFMAs of step s run, and the previous group's sums are scaled into the
@@ -182,7 +183,7 @@ __global__ void __launch_bounds__(64 * QWAVES) k_gemm_q4(const uint16_t* __restr
 #pragma unroll
         for (int q = 0; q < NA; ++q) lds_dma16(asrc[q] + (size_t)g * QK, stg + adst[q]);
 #pragma unroll
-        for (int i = 0; i < WPL; ++i) wr[i] = wbase[(size_t)g * (64 * WPL) + 64 * i];
+        for (int i = 0; i < WPL; ++i) wr[i] = __builtin_nontemporal_load(wbase + (size_t)g * (64 * WPL) + 64 * i);
     };
 
     floatx16 acc[MT], tmp[2][MT];
