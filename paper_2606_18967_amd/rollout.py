@@ -26,6 +26,14 @@ sequences leave the batch through the slot list (no KV moves), so the live
 batch shrinks as in the paper's long tail.  The prompt is a random KV context
 of `prompt` positions per sequence, the same for every policy, so the
 makespan measured is that of the decode phase.
+
+With graphs on, the live batch of each iteration is padded up to a bucket (a
+multiple of BUCKET rows; the padding rows run on spare KV slots whose length
+is reset before every step) and each (bucket, draft length) SD step and each
+AR bucket is captured once as a HIP graph and replayed afterwards, as serving
+engines pre-capture graphs per batch size (Sec. 4.1).  The first iteration at
+a new bucket runs the padded step eagerly and captures it; capture time is
+reported apart from the makespan.
 """
 from __future__ import annotations
 
@@ -40,6 +48,14 @@ import numpy as np
 from . import sdrl, synth
 
 POLICIES = ("ar", "sd", "toggle", "adaptive")
+BUCKET = 8                         # graph buckets: live batches padded to a multiple of this many rows
+
+
+def bucket_of(n: int, step: int = BUCKET) -> int:
+    """The bucket (padded batch size) of a live batch of n rows."""
+    if n < 1:
+        raise ValueError("a bucket holds at least one row")
+    return (n + step - 1) // step * step
 GAMMA_SET = (5, 7, 9, 11)          # Gamma, alpha_up, alpha_down, P and eps as the paper sets them (App. E.3)
 A_UP, A_DOWN, PATIENCE, EPS = 0.94, 0.85, 2, 0.05
 
@@ -66,6 +82,8 @@ class RolloutResult:
     switch_iter: int | None             # iteration at which SD switched on
     switch_B: int | None
     trace: list = field(default_factory=list)   # (mode, B, S_mean, ms, emitted) per iteration
+    graphs: int = 0                     # HIP graphs captured during the rollout
+    capture_s: float = 0.0              # their capture time (outside makespan_s)
 
 
 def decode(lengths: np.ndarray, prompt: int, policy: str, gamma: int, tau_prev: float, cost, eps: float,
@@ -98,14 +116,20 @@ def decode(lengths: np.ndarray, prompt: int, policy: str, gamma: int, tau_prev: 
                 st["switch_iter"], st["switch_B"] = it, Bl
         t0 = clock()
         if sd_on:
-            n = np.asarray(sd_fn(gamma), dtype=np.int64)
+            r = sd_fn(gamma)
+        else:
+            r = ar_fn()
+        # an iteration function may return (tokens, seconds spent capturing a graph)
+        n, cap = (r if isinstance(r, tuple) else (r, 0.0))
+        n = np.asarray(n, dtype=np.int64)
+        if sd_on:
             st["sd_iters"] += 1
             st["sd_tokens"] += int(n.sum())
             st["sd_rows"] += Bl
         else:
-            n = np.asarray(ar_fn(), dtype=np.int64)
             st["ar_iters"] += 1
-        dt = clock() - t0
+        dt = clock() - t0 - cap
+        st["capture_s"] = st.get("capture_s", 0.0) + cap
         total += dt
         if n.shape != (Bl,) or (n < 1).any():
             raise RuntimeError("a decode iteration must emit at least one token per live row")
@@ -130,12 +154,17 @@ class Rollout:
     viewed at the live batch size and draft length of each iteration."""
 
     def __init__(self, cfg: dict, B: int, prompt: int, lmax: int, gmax: int = max(GAMMA_SET), seed: int = 3,
-                 T: float = 1.0, fmt: str = "w4"):
+                 T: float = 1.0, fmt: str = "w4", graphs: bool = False, padded: bool | None = None):
         import torch
         self.torch = torch
         self.cfg, self.B, self.prompt, self.gmax, self.seed, self.T, self.fmt = cfg, B, prompt, gmax, seed, T, fmt
+        # padded: steps run at the bucket size (spare slots B .. B + BUCKET - 2 carry the padding rows);
+        # graphs: the padded steps are captured and replayed
+        self.graphs = graphs
+        self.padded = graphs if padded is None else (padded or graphs)
+        self.spare = BUCKET - 1 if self.padded else 0
         self.dev = torch.device("cuda", 0)
-        self.eng = sdrl.Engine(cfg, B, prompt + lmax + gmax + 2, gmax)
+        self.eng = sdrl.Engine(cfg, B + self.spare, prompt + lmax + gmax + 2, gmax)
         self.W = synth.make_weights(cfg, seed, self.dev)
         self.eng.bind_weights(self.W)
         self.k, self.v, self.kv_len = self.eng.alloc_kv()
@@ -143,6 +172,7 @@ class Rollout:
         synth.fill_kv_context(self.k, self.v, prompt, seed + 100)
         self.qbuf = self.eng.refresh_drafter(fmt=fmt)
         V, dev, i32, f32 = cfg["vocab"], self.dev, torch.int32, torch.float32
+        B = B + self.spare
         self.flat = dict(draft_tok=torch.zeros(B * gmax, dtype=i32, device=dev),
                          q_logits=torch.zeros(B * gmax * V, dtype=f32, device=dev),
                          q_stats=torch.zeros(B * gmax * 2, dtype=f32, device=dev),
@@ -175,6 +205,73 @@ class Rollout:
         state = dict(slots=torch.arange(self.B, dtype=torch.int32, device=self.dev),
                      last=synth.make_tokens(self.B, 1, V, self.seed + 7 + step)[:, 0].to(self.dev).contiguous())
         T, seed = self.T, self.seed
+        cache = {}                             # (kind, bucket, gamma) -> padded buffers and captured graph
+        spare = torch.arange(self.B, self.B + self.spare, dtype=torch.int32, device=self.dev)
+
+        def padded_entry(kind, Bl, g):
+            bk = bucket_of(Bl)
+            key = (kind, bk, g)
+            ent = cache.get(key)
+            if ent is None:
+                ent = dict(slots=torch.zeros(bk, dtype=torch.int32, device=self.dev),
+                           last=torch.zeros(bk, dtype=torch.int32, device=self.dev), graph=None)
+                if kind == "sd":
+                    ent["bufs"] = sdrl.SDBuffers(eng, bk, g)
+                else:
+                    ent["out"] = torch.zeros(bk, dtype=torch.int32, device=self.dev)
+                    ent["logits"] = torch.zeros((bk, V), dtype=torch.float32, device=self.dev)
+                cache[key] = ent
+            # live rows first, then the spare slots; the spare slots restart from the prompt every step
+            ent["slots"][:Bl].copy_(state["slots"])
+            ent["slots"][Bl:].copy_(spare[:bk - Bl])
+            ent["last"][:Bl].copy_(state["last"])
+            ent["last"][Bl:].zero_()
+            self.kv_len[self.B:].fill_(self.prompt)
+            return ent
+
+        def run_padded(ent, eager, capture):
+            """Replays the entry's graph, or runs the step eagerly (and captures it)."""
+            if ent["graph"] is not None:
+                ent["graph"].replay()
+                return 0.0
+            eager()
+            if not capture:
+                return 0.0
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            graph = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream(device=self.dev)          # default priority
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.graph(graph, stream=side):
+                eager()
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            ent["graph"] = graph
+            return time.perf_counter() - t0
+
+        def ar_padded():
+            Bl = state["slots"].numel()
+            ent = padded_entry("ar", Bl, 0)
+
+            def eager():
+                eng.ar_step(ent["slots"], ent["last"], T, seed, 2 * step, ent["out"], ent["logits"])
+                torch.add(ent["out"], 0, out=ent["last"])      # a kernel node, not a copy node
+            cap = run_padded(ent, eager, self.graphs)
+            state["last"] = ent["last"][:Bl].clone()
+            torch.cuda.synchronize()
+            return np.ones(Bl, dtype=np.int64), cap
+
+        def sd_padded(g):
+            Bl = state["slots"].numel()
+            ent = padded_entry("sd", Bl, g)
+            bufs = ent["bufs"]
+
+            def eager():
+                sdrl.sd_step(eng, bufs, ent["slots"], ent["last"], T, seed, 2 * step + 1)
+                torch.add(bufs.next_tok, 0, out=ent["last"])
+            cap = run_padded(ent, eager, self.graphs)
+            state["last"] = ent["last"][:Bl].clone()
+            return bufs.n_emit[:Bl].cpu().numpy(), cap
 
         def ar_fn():
             Bl = state["slots"].numel()
@@ -202,13 +299,16 @@ class Rollout:
             state["last"] = state["last"].index_select(0, idx)
 
         torch.cuda.synchronize()
-        st = decode(lengths, self.prompt, policy, gamma, tau_prev, cost, eps, ar_fn, sd_fn, compact_fn,
+        st = decode(lengths, self.prompt, policy, gamma, tau_prev, cost, eps,
+                    ar_padded if self.padded else ar_fn, sd_padded if self.padded else sd_fn, compact_fn,
                     keep_trace=keep_trace)
         eng.sync()
         res = RolloutResult(policy=policy, step=step, gamma=gamma, tau_prev=tau_prev, tau=st["tau"],
                             makespan_s=st["makespan_s"], prep_ms=prep_ms, ar_iters=st["ar_iters"],
                             sd_iters=st["sd_iters"], tokens=int(np.asarray(lengths).sum()),
-                            switch_iter=st["switch_iter"], switch_B=st["switch_B"], trace=st["trace"])
+                            switch_iter=st["switch_iter"], switch_B=st["switch_B"], trace=st["trace"],
+                            graphs=sum(e["graph"] is not None for e in cache.values()),
+                            capture_s=st.get("capture_s", 0.0))
         return res, st
 
     def close(self):
@@ -288,6 +388,9 @@ def main(argv=None):
     ap.add_argument("--calib", default="", help="calibrate.py --out JSON; default: calibrate now on this model")
     ap.add_argument("--calib-B", default="1,4,16,64,128")
     ap.add_argument("--calib-S", default="512,2048,4096")
+    ap.add_argument("--graphs", action="store_true",
+                    help="pad live batches to buckets of BUCKET rows and replay one captured HIP graph per "
+                         "(bucket, draft length) and per AR bucket")
     ap.add_argument("--tau-carry", action="store_true",
                     help="carry the toggle's tau to a new draft length through the acceptance rate "
                          "(default: Algorithm 1 as written, the measured tau as it is)")
@@ -307,7 +410,7 @@ def main(argv=None):
         calib = dict(F_eff=calib["F_eff"], params=calib["params"], agreement=calib["agreement"])
     cost = calibrated_cost(cfg, calib)
     log("building the rollout engine ...")
-    ro = Rollout(cfg, a.B, a.prompt, a.lmax, seed=a.seed, fmt=a.drafter)
+    ro = Rollout(cfg, a.B, a.prompt, a.lmax, seed=a.seed, fmt=a.drafter, graphs=a.graphs)
     lengths_fn = lambda t: response_lengths(a.B, a.median, a.sigma, a.lmin, a.lmax, a.seed * 1000 + t)
     # one untimed rollout to load every kernel
     ro.run("sd", GAMMA_SET[0], float(GAMMA_SET[0]), cost, EPS, np.minimum(lengths_fn(0), 64), 99, keep_trace=False)
@@ -319,10 +422,12 @@ def main(argv=None):
         for r in rs:
             log(f"{pol:9s} step {r.step}: gamma {r.gamma:2d}  tau_prev {r.tau_prev:5.2f}  tau "
                 f"{'  -  ' if r.tau is None else f'{r.tau:5.2f}'}  makespan {r.makespan_s:7.3f} s  "
-                f"AR iters {r.ar_iters:5d}  SD iters {r.sd_iters:5d}  SD on at B={r.switch_B}  prep {r.prep_ms:.1f} ms")
+                f"AR iters {r.ar_iters:5d}  SD iters {r.sd_iters:5d}  SD on at B={r.switch_B}  prep {r.prep_ms:.1f} ms"
+                f"  graphs {r.graphs} ({r.capture_s:.2f} s to capture)")
     ro.close()
     L0 = lengths_fn(0)
     summary = dict(model=cfg["name"], drafter=a.drafter, B=a.B, prompt=a.prompt, tau_carry=a.tau_carry,
+                   graphs=a.graphs,
                    lengths=dict(median=a.median, sigma=a.sigma, lo=a.lmin, hi=a.lmax, mean_step0=float(L0.mean()),
                                 max_step0=int(L0.max())),
                    calib=dict(F_eff=calib["F_eff"], params=calib["params"]),
@@ -331,7 +436,7 @@ def main(argv=None):
     if a.out:
         with open(a.out, "w") as fh:
             json.dump(summary, fh)
-    print(json.dumps(dict(model=summary["model"], drafter=a.drafter, B=a.B, tau_carry=a.tau_carry,
+    print(json.dumps(dict(model=summary["model"], drafter=a.drafter, B=a.B, tau_carry=a.tau_carry, graphs=a.graphs,
                           makespan_s=summary["makespan_s"],
                           tau={p: [r.tau for r in rs] for p, rs in results.items()},
                           gamma={p: [r.gamma for r in rs] for p, rs in results.items()},

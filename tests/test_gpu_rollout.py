@@ -54,3 +54,32 @@ def test_tiny_rollout_is_reproducible(tiny_rollout):
     assert [t[4] for t in a[0].trace] == [t[4] for t in b[0].trace]
     c = ro.run("sd", 5, 5.0, cost, 0.05, L, step=4)               # another training step draws afresh
     assert c[0].tau is not None
+
+
+@pytest.mark.parametrize("policy,gamma", [("ar", 5), ("sd", 5), ("toggle", 7)])
+def test_graph_rollout_equals_padded_eager_rollout(policy, gamma):
+    """The long-tail driver with per-(bucket, draft length) HIP graphs: live
+    batches padded to buckets of 8 rows (spare slots carry the padding), each
+    bucket's step captured once and replayed.  Every replay must give exactly
+    the tokens of the same padded step run eagerly, and every live slot's
+    cache length must end at prompt + the tokens it emitted."""
+    import torch
+    from paper_2606_18967_amd import rollout, sdrl
+    torch.cuda.set_device(0)
+    cfg = rollout.MODELS["TINY_BF16"]
+    L = np.array([3, 30, 1, 17, 9, 12, 25, 5, 21, 14, 2])      # 11 sequences: buckets 16 and 8
+    say(f"graph rollout policy={policy} gamma={gamma}")
+    runs = []
+    for graphs in (True, False):
+        ro = rollout.Rollout(cfg, B=len(L), prompt=16, lmax=40, seed=9, graphs=graphs, padded=True)
+        res, st = ro.run(policy, gamma, 5.0, sdrl.cost_init(ro.cfg), 0.05, L, step=2)
+        kv = ro.kv_len[:ro.B].cpu().numpy()
+        assert (kv - ro.prompt == st["gen"]).all()
+        assert (st["gen"] >= L).all()
+        runs.append((res, st))
+        ro.close()
+    (rg, sg), (re_, se) = runs
+    assert (sg["gen"] == se["gen"]).all()
+    assert [t[4] for t in rg.trace] == [t[4] for t in re_.trace]
+    assert [t[:2] for t in rg.trace] == [t[:2] for t in re_.trace]
+    assert rg.graphs >= 2 and re_.graphs == 0

@@ -180,3 +180,24 @@ def test_calibrated_cost_takes_the_fitted_terms():
     base = sdrl.cost_init(synth.L4_8B)
     assert m.F_eff == 7.0e14 and m.BW_eff == 5.0e12 and m.c_V == 3e-6
     assert m.W_T == base.W_T and m.kappa_th == base.kappa_th
+
+
+def test_buckets_pad_to_multiples():
+    assert [rollout.bucket_of(n) for n in (1, 7, 8, 9, 16, 17, 128)] == [8, 8, 8, 16, 16, 24, 128]
+    with pytest.raises(ValueError):
+        rollout.bucket_of(0)
+
+
+def test_capture_time_is_kept_out_of_the_makespan():
+    """An iteration that returns (tokens, capture seconds) is timed without
+    its capture; the capture time is accumulated apart."""
+    clock = iter([0.0, 1.0, 1.5, 2.5]).__next__
+    outs = [(np.array([2, 3]), 0.75), np.array([3])]
+
+    def sd_fn(g):
+        return outs.pop(0)
+
+    st = rollout.decode(np.array([5, 3]), 10, "sd", 4, 5.0, None, 0.05, lambda: None, sd_fn, lambda keep: None,
+                        clock=clock)
+    assert st["sd_iters"] == 2 and st["capture_s"] == 0.75
+    assert st["makespan_s"] == pytest.approx(0.25 + 1.0)
