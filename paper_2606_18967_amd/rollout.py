@@ -24,7 +24,8 @@ with means of 620-660; a few long ones set the completion time, Sec. 3.3
 and App. A).  A response finishes when it has emitted its length; finished
 sequences leave the batch through the slot list (no KV moves), so the live
 batch shrinks as in the paper's long tail.  The prompt is a random KV context
-of `prompt` positions per sequence, the same for every policy, so the
+of `prompt` positions per sequence (or, with --prefill, `prompt` random
+tokens prefilled through the target), the same for every policy, so the
 makespan measured is that of the decode phase.
 
 With graphs on, the live batch of each iteration is padded up to a bucket (a
@@ -154,7 +155,8 @@ class Rollout:
     viewed at the live batch size and draft length of each iteration."""
 
     def __init__(self, cfg: dict, B: int, prompt: int, lmax: int, gmax: int = max(GAMMA_SET), seed: int = 3,
-                 T: float = 1.0, fmt: str = "w4", graphs: bool = False, padded: bool | None = None):
+                 T: float = 1.0, fmt: str = "w4", graphs: bool = False, padded: bool | None = None,
+                 prefill: bool = False):
         import torch
         self.torch = torch
         self.cfg, self.B, self.prompt, self.gmax, self.seed, self.T, self.fmt = cfg, B, prompt, gmax, seed, T, fmt
@@ -169,7 +171,19 @@ class Rollout:
         self.eng.bind_weights(self.W)
         self.k, self.v, self.kv_len = self.eng.alloc_kv()
         self.eng.bind_kv(self.k, self.v, self.kv_len)
-        synth.fill_kv_context(self.k, self.v, prompt, seed + 100)
+        self.prefill_s = None
+        if prefill:
+            # real prompts: `prompt` random tokens per sequence through the target (every slot, spares too)
+            nslots = B + self.spare
+            toks = synth.make_tokens(nslots, prompt, cfg["vocab"], seed + 5).to(self.dev).contiguous()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            self.eng.prefill(torch.arange(nslots, dtype=torch.int32, device=self.dev), toks)
+            self.eng.sync()
+            self.prefill_s = time.perf_counter() - t0
+            del toks
+        else:
+            synth.fill_kv_context(self.k, self.v, prompt, seed + 100)
         self.qbuf = self.eng.refresh_drafter(fmt=fmt)
         V, dev, i32, f32 = cfg["vocab"], self.dev, torch.int32, torch.float32
         B = B + self.spare
@@ -388,6 +402,8 @@ def main(argv=None):
     ap.add_argument("--calib", default="", help="calibrate.py --out JSON; default: calibrate now on this model")
     ap.add_argument("--calib-B", default="1,4,16,64,128")
     ap.add_argument("--calib-S", default="512,2048,4096")
+    ap.add_argument("--prefill", action="store_true",
+                    help="prefill `prompt` random tokens per sequence through the target instead of random KV context")
     ap.add_argument("--graphs", action="store_true",
                     help="pad live batches to buckets of BUCKET rows and replay one captured HIP graph per "
                          "(bucket, draft length) and per AR bucket")
@@ -410,7 +426,9 @@ def main(argv=None):
         calib = dict(F_eff=calib["F_eff"], params=calib["params"], agreement=calib["agreement"])
     cost = calibrated_cost(cfg, calib)
     log("building the rollout engine ...")
-    ro = Rollout(cfg, a.B, a.prompt, a.lmax, seed=a.seed, fmt=a.drafter, graphs=a.graphs)
+    ro = Rollout(cfg, a.B, a.prompt, a.lmax, seed=a.seed, fmt=a.drafter, graphs=a.graphs, prefill=a.prefill)
+    if ro.prefill_s is not None:
+        log(f"prefill of {a.B} x {a.prompt} tokens: {ro.prefill_s:.2f} s")
     lengths_fn = lambda t: response_lengths(a.B, a.median, a.sigma, a.lmin, a.lmax, a.seed * 1000 + t)
     # one untimed rollout to load every kernel
     ro.run("sd", GAMMA_SET[0], float(GAMMA_SET[0]), cost, EPS, np.minimum(lengths_fn(0), 64), 99, keep_trace=False)
@@ -427,7 +445,7 @@ def main(argv=None):
     ro.close()
     L0 = lengths_fn(0)
     summary = dict(model=cfg["name"], drafter=a.drafter, B=a.B, prompt=a.prompt, tau_carry=a.tau_carry,
-                   graphs=a.graphs,
+                   graphs=a.graphs, prefill_s=ro.prefill_s,
                    lengths=dict(median=a.median, sigma=a.sigma, lo=a.lmin, hi=a.lmax, mean_step0=float(L0.mean()),
                                 max_step0=int(L0.max())),
                    calib=dict(F_eff=calib["F_eff"], params=calib["params"]),

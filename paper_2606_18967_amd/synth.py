@@ -16,7 +16,7 @@ from __future__ import annotations
 
 import torch
 
-# Llama-style decoders; rope_theta 1e4 for the tiny model, 5e5 for the 8B/32B shapes.
+# Llama-style decoders; rope_theta 1e4 for the tiny model, 5e5 for the 8B shape, 1e6 for the 32B shape.
 TINY = dict(name="tiny-2L-h256", n_layers=2, hidden=256, n_q=4, n_kv=4, head_dim=64, ffn=1024, vocab=512,
             dtype="f32", rope_theta=10000.0, rms_eps=1e-5)
 L4_8B = dict(name="8B-shape-4L", n_layers=4, hidden=4096, n_q=32, n_kv=8, head_dim=128, ffn=14336, vocab=128256,
