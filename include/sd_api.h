@@ -183,6 +183,20 @@ sd_status sd_refresh_drafter(sd_engine e, void* qbuf, size_t bytes, void* stream
 sd_status sd_prefill(sd_engine e, int32_t B, const int32_t* slots, const int32_t* tokens, int32_t n,
                      void* stream);
 
+/* Target prefill of prompts of different lengths (the rollout's prompts,
+ * Sec. 5.1; every decoding step then starts from each sequence's own
+ * kv_len, App. D.1): caches tokens[b*ld + i] for i < len[b] (tokens: device
+ * int32[B][ld], row b's entries past len[b] are never read) of sequence
+ * slots[b] at positions kv_len + i, then kv_len += len[b].  len: device
+ * int32[B] with 0 <= len[b] <= ld.  The batch runs in rounds of a common
+ * number of positions; a sequence whose prompt has ended computes padding
+ * rows that are neither cached nor counted.  Errors: SD_E_INVAL (NULL
+ * pointers, ld outside [1, max_ctx]), SD_E_STATE; a length outside [0, ld]
+ * is reported by sd_sync (and that sequence is left unchanged), as are bad
+ * slots, token ids and positions past max_ctx. */
+sd_status sd_prefill_ragged(sd_engine e, int32_t B, const int32_t* slots, const int32_t* tokens, int32_t ld,
+                            const int32_t* len, void* stream);
+
 /* Draft (Algorithm 1's SD branch, App. D.1): for j = 1..gamma the drafter
  * runs x_{j-1} (x_0 = last_tok[b]) at position kv_len + j - 1, writes
  * provisional KV there, and draws d_j ~ softmax(q_j / temperature) by
@@ -225,7 +239,7 @@ sd_status sd_accept(sd_engine e, int32_t B, const int32_t* slots, const int32_t*
  * [0, max_slots)).  All other arguments, layouts and outputs as sd_accept.
  * Scratch: the kernels' partial results live in a static device array of
  * 2^20 floats (4 MiB) per GPU, held until the process ends; a call needs
- * B*(gamma+1)*C*2 + B*C*4 + 6*B + 4 floats with C = ceil(vocab / 4096)
+ * B*(gamma+1)*C*2 + B*C*4 + 6*B + 5 floats with C = ceil(vocab / 4096)
  * vocabulary chunks, and a larger one returns SD_E_INVAL before launching
  * anything.  Every call on a GPU shares that GPU's array: calls whose work
  * overlaps on one GPU (different streams, or threads) race and must not be

@@ -94,6 +94,37 @@ enum : int {
     ERR_TOKEN = 1,      // token id outside [0, vocab)
     ERR_CTX = 2,        // a position at or beyond max_ctx
     ERR_PAGE = 3,       // a block-table entry outside [0, n_pages) (paged KV)
-    ERR_COUNT = 4
+    ERR_LEN = 4,        // a prefill length outside [0, row width]
+    ERR_COUNT = 5
 };
+// v + P[0][idx] + P[1][idx] + ... + P[S - 1][idx] (split stride st floats),
+// added in split order.  The loads of eight splits go out before their adds,
+// so their memory round trips overlap; past the last split the loads repeat
+// split S - 1 (in bounds, never added).
+__device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+__device__ __forceinline__ float add_splits(float v, const float* P, int S, size_t st, size_t idx)
+{
+    for (int s0 = 0; s0 < S; s0 += 8) {
+        float p[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) p[u] = P[(size_t)min(s0 + u, S - 1) * st + idx];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s0 + u < S) v += p[u];
+    }
+    return v;
+}
+__device__ __forceinline__ float4 add_splits(float4 v, const float* P, int S, size_t st, size_t idx)
+{
+    for (int s0 = 0; s0 < S; s0 += 8) {
+        float4 p[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) p[u] = *(const float4*)(P + (size_t)min(s0 + u, S - 1) * st + idx);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s0 + u < S) v = add4(v, p[u]);
+    }
+    return v;
+}
+
 __device__ __forceinline__ void flag_error(uint32_t* err, int kind) { ((volatile uint32_t*)err)[kind] = 1u; }

@@ -83,6 +83,7 @@ struct sd_engine_s {
     float* acc_work = nullptr;
     float2* rope = nullptr;
     uint32_t* err = nullptr;
+    int32_t* pf_lim = nullptr;   // [max_slots] rows of one ragged-prefill round
     float* gpart = nullptr;      // split-K partial sums
     size_t gpart_cap = 0;        // floats
     int launch_err = 0;          // a GEMM shape the kernels refused (reported by sd_sync)
@@ -234,7 +235,7 @@ static size_t gpart_bytes(const sd_model_cfg& c, int R)
 static void free_ws(sd_engine e)
 {
     void* ps[] = {e->h, e->a, e->qkv, e->qrot, e->att, e->gu, e->act, e->att_part, e->samp_part, e->acc_work, e->rope, e->err,
-                  e->gpart};
+                  e->pf_lim, e->gpart};
     for (void* p : ps)
         if (p) (void)hipFree(p);
 }
@@ -277,6 +278,7 @@ extern "C" sd_status sd_create(const sd_model_cfg* cfg, int32_t max_slots, int32
         {(void**)&e->acc_work, accept_work_floats(max_slots, max_gamma) * 4},
         {(void**)&e->rope, (size_t)max_ctx * (c.head_dim / 2) * sizeof(float2)},
         {(void**)&e->err, ERR_COUNT * 4},
+        {(void**)&e->pf_lim, (size_t)max_slots * 4},
         {(void**)&e->gpart, gpart_bytes(c, e->rows_max)},
     };
     e->gpart_cap = gpart_bytes(c, e->rows_max) / 4;
@@ -463,10 +465,12 @@ static bool proj_swiglu(sd_engine e, bool draft, int layer, const void* A, void*
 // tokB[b*sB + i - 1].  If logits != NULL, row r's logits go to logits + r*ldl;
 // otherwise the last layer's FFN (which only feeds the logits) is skipped.
 static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const int32_t* tokA, int sA,
-                    const int32_t* tokB, int sB, int n, int off, float* logits, long ldl, hipStream_t s)
+                    const int32_t* tokB, int sB, int n, int off, float* logits, long ldl, hipStream_t s,
+                    const int32_t* lim = nullptr)
 {
     const sd_model_cfg& c = e->c;
     rows_t r = {B, n, off, slots, e->kv_len, e->max_slots, e->max_ctx, e->err};
+    r.lim = lim;
     cache_t kv = {e->k, e->v, e->f32 ? 1 : 0, c.n_kv, c.head_dim, e->geo};
     const int R = B * n;
     const act_t at = act_of(e, draft);
@@ -532,6 +536,26 @@ extern "C" sd_status sd_prefill(sd_engine e, int32_t B, const int32_t* slots, co
         launch_kv_advance(B, slots, nullptr, nc, e->kv_len, e->max_slots, e->err, s);
     }
     return launched("sd_prefill");
+}
+
+extern "C" sd_status sd_prefill_ragged(sd_engine e, int32_t B, const int32_t* slots, const int32_t* tokens, int32_t ld,
+                                       const int32_t* len, void* stream)
+{
+    sd_status st = check_step(e, B, slots, false);
+    if (st != SD_OK) return st;
+    if (!tokens || !len) return fail(SD_E_INVAL, "NULL tokens or len");
+    if (ld < 1 || ld > e->max_ctx) return fail(SD_E_INVAL, "ld=%d outside [1, max_ctx=%d]", ld, e->max_ctx);
+    hipStream_t s = (hipStream_t)stream;
+    // rounds of nc positions for the whole batch; row (b, i) of a round is
+    // padding once sequence b has no token left (i >= lim[b])
+    int chunk = e->rows_max / B;
+    for (int t0 = 0; t0 < ld; t0 += chunk) {
+        int nc = ld - t0 < chunk ? ld - t0 : chunk;
+        launch_prefill_lim(B, len, t0, nc, ld, e->pf_lim, e->err, s);
+        forward(e, false, B, slots, tokens + t0, ld, tokens + t0 + 1, ld, nc, 0, nullptr, 0, s, e->pf_lim);
+        launch_kv_advance(B, slots, e->pf_lim, 0, e->kv_len, e->max_slots, e->err, s);
+    }
+    return launched("sd_prefill_ragged");
 }
 
 static sd_status check_gamma(sd_engine e, int gamma, float T)
@@ -697,6 +721,7 @@ extern "C" sd_status sd_sync(sd_engine e, void* stream)
     if (flags[ERR_SLOT]) return fail(SD_E_INVAL, "device: slot index outside [0, max_slots)");
     if (flags[ERR_TOKEN]) return fail(SD_E_INVAL, "device: token id outside [0, vocab)");
     if (flags[ERR_CTX]) return fail(SD_E_INVAL, "device: position at or beyond max_ctx");
+    if (flags[ERR_LEN]) return fail(SD_E_INVAL, "device: prefill length outside [0, ld]");
     if (flags[ERR_PAGE]) return fail(SD_E_INVAL, "device: block-table entry outside [0, n_pages)");
     if (e->launch_err) { e->launch_err = 0; return fail(SD_E_UNSUPPORTED, "an int4 GEMM shape was refused"); }
     return SD_OK;

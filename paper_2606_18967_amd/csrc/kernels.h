@@ -16,6 +16,7 @@ struct rows_t {
     const int32_t* kv_len;  // device [max_slots]
     int max_slots, max_ctx;
     uint32_t* err;          // device error words
+    const int32_t* lim = nullptr;   // device [B] or NULL: rows (b, i >= lim[b]) are padding, skipped silently
 };
 
 // KV cache geometry.  The element offset of (slot, layer, KV head h,
@@ -68,6 +69,9 @@ int attention_chunk();
 void launch_silu_mul(const float* gu, const float* P, int S, int R, int F, void* out, act_t out_t, hipStream_t s);
 void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_const,
                        int32_t* kv_len, int max_slots, uint32_t* err, hipStream_t s);
+// lim[b] = clamp(len[b] - t0, 0, nc) for one round of a ragged prefill; a
+// length outside [0, ld] sets ERR_LEN and counts as 0
+void launch_prefill_lim(int B, const int32_t* len, int t0, int nc, int ld, int32_t* lim, uint32_t* err, hipStream_t s);
 void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int span,
                       const cache_t& c, int n_layers, int max_slots, int max_ctx, hipStream_t s);
 

@@ -649,8 +649,7 @@ __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__
     size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
     size_t MN = (size_t)M * N;
     if (idx >= MN) return;
-    float v = 0.f;
-    for (int s = 0; s < S; ++s) v += P[(size_t)s * MN + idx];
+    const float v = add_splits(0.f, P, S, MN, idx);
     int row = (int)(idx / N), col = (int)(idx % N);
     float* cp = C + (size_t)row * ldc + col;
     *cp = mode == GEMM_ADD ? *cp + v : v;

@@ -72,7 +72,8 @@ __global__ void __launch_bounds__(1024) k_embed_rmsnorm(rows_t r, const int32_t*
     __shared__ float red[16];
     const int row = blockIdx.x;
     const int b = row / r.n, i = row - b * r.n;
-    const int tok = (i == 0) ? tokA[(size_t)b * sA] : tokB[(size_t)b * sB + i - 1];
+    const bool pad = r.lim && i >= r.lim[b];            // a padding row: embedded as token 0, never cached
+    const int tok = pad ? 0 : (i == 0) ? tokA[(size_t)b * sA] : tokB[(size_t)b * sB + i - 1];
     const bool ok = tok >= 0 && tok < V;
     if (!ok && threadIdx.x == 0) flag_error(r.err, ERR_TOKEN);
     const T* er = E + (size_t)(ok ? tok : 0) * H;
@@ -106,10 +107,7 @@ __global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, 
     for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
         float4 x = *(const float4*)(hr + k4);
         if (S > 1) {
-            for (int sp = 0; sp < S; ++sp) {
-                const float4 p = *(const float4*)(P + sp * RH + (size_t)row * H + k4);
-                x.x += p.x; x.y += p.y; x.z += p.z; x.w += p.w;
-            }
+            x = add_splits(x, P, S, RH, (size_t)row * H + k4);
             *(float4*)(hr + k4) = x;
         }
         ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
@@ -126,9 +124,7 @@ __global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, 
 __device__ __forceinline__ float sum_parts(const float* src, const float* P, int S, size_t RN, size_t idx)
 {
     if (S <= 1) return src[idx];
-    float v = 0.f;
-    for (int sp = 0; sp < S; ++sp) v += P[sp * RN + idx];
-    return v;
+    return add_splits(0.f, P, S, RN, idx);
 }
 
 // ------------------------------------------------------------------ rope + kv write
@@ -151,8 +147,9 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
     const size_t RN = (size_t)r.B * r.n * units * d;
     const size_t base_idx = (size_t)row * units * d;
     float* qo = q_out + (size_t)row * n_q * d;
-    if (!ok) {
-        if (threadIdx.x == 0 && blockIdx.y == 0) {
+    const bool pad = r.lim && (row % r.n) >= r.lim[row / r.n];   // padding rows are not cached
+    if (!ok || pad) {
+        if (!pad && threadIdx.x == 0 && blockIdx.y == 0) {
             const bool bad_slot = slot < 0 || slot >= r.max_slots;
             flag_error(r.err, bad_slot ? ERR_SLOT : ERR_CTX);
         }
@@ -655,13 +652,39 @@ __global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int 
     int nch = (ctx + chunk - 1) / chunk;
     if (nch > max_chunks) nch = max_chunks;
     const float* pp = part + ((size_t)row * n_q + hq) * max_chunks * (D + 2);
+    // chunks are merged in order; the loads of eight chunks go out together
+    // (past the last chunk they repeat chunk nch - 1 and are not used)
     for (int k = threadIdx.x; k < D; k += blockDim.x) {
         float mm = -INFINITY;
-        for (int c = 0; c < nch; ++c) if (pp[c * (D + 2) + 1] > 0.f) mm = fmaxf(mm, pp[c * (D + 2)]);
+        for (int c0 = 0; c0 < nch; c0 += 8) {
+            float cm[8], cl[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float* pc = pp + (size_t)min(c0 + u, nch - 1) * (D + 2);
+                cm[u] = pc[0];
+                cl[u] = pc[1];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (c0 + u < nch && cl[u] > 0.f) mm = fmaxf(mm, cm[u]);
+        }
         float ls = 0.f, os = 0.f;
-        for (int c = 0; c < nch; ++c) {
-            const float* pc = pp + c * (D + 2);
-            if (pc[1] > 0.f) { float f = __expf(pc[0] - mm); ls += pc[1] * f; os += pc[2 + k] * f; }
+        for (int c0 = 0; c0 < nch; c0 += 8) {
+            float cm[8], cl[8], co[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float* pc = pp + (size_t)min(c0 + u, nch - 1) * (D + 2);
+                cm[u] = pc[0];
+                cl[u] = pc[1];
+                co[u] = pc[2 + k];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (c0 + u < nch && cl[u] > 0.f) {
+                    const float f = __expf(cm[u] - mm);
+                    ls += cl[u] * f;
+                    os += co[u] * f;
+                }
         }
         store_act<O>(out, ((size_t)row * n_q + hq) * D + k, ls > 0.f ? os / ls : 0.f);
     }
@@ -682,13 +705,8 @@ __global__ void __launch_bounds__(256) k_silu_mul(const float* gu, const float* 
         g = *(const float4*)(gu + gi);
         u = *(const float4*)(gu + ui);
     } else {
-        g = make_float4(0.f, 0.f, 0.f, 0.f);
-        u = g;
-        for (int sp = 0; sp < S; ++sp) {
-            const float4 a = *(const float4*)(P + sp * RN + gi), c = *(const float4*)(P + sp * RN + ui);
-            g.x += a.x; g.y += a.y; g.z += a.z; g.w += a.w;
-            u.x += c.x; u.y += c.y; u.z += c.z; u.w += c.w;
-        }
+        g = add_splits(make_float4(0.f, 0.f, 0.f, 0.f), P, S, RN, gi);
+        u = add_splits(make_float4(0.f, 0.f, 0.f, 0.f), P, S, RN, ui);
     }
     const size_t o = (size_t)row * F + f;
     store_act<O>(out, o, g.x / (1.f + __expf(-g.x)) * u.x);
@@ -706,6 +724,18 @@ __global__ void k_kv_advance(int B, const int32_t* slots, const int32_t* inc, in
     int s = slots[b];
     if (s < 0 || s >= max_slots) { flag_error(err, ERR_SLOT); return; }
     kv_len[s] += inc ? inc[b] : inc_const;
+}
+
+__global__ void k_prefill_lim(int B, const int32_t* len, int t0, int nc, int ld, int32_t* lim, uint32_t* err)
+{
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    int n = len[b];
+    if (n < 0 || n > ld) {
+        flag_error(err, ERR_LEN);
+        n = 0;
+    }
+    lim[b] = min(max(n - t0, 0), nc);
 }
 
 template <typename T>
@@ -884,6 +914,11 @@ void launch_kv_advance(int B, const int32_t* slots, const int32_t* inc, int inc_
                        int max_slots, uint32_t* err, hipStream_t s)
 {
     k_kv_advance<<<(B + 255) / 256, 256, 0, s>>>(B, slots, inc, inc_const, kv_len, max_slots, err);
+}
+
+void launch_prefill_lim(int B, const int32_t* len, int t0, int nc, int ld, int32_t* lim, uint32_t* err, hipStream_t s)
+{
+    k_prefill_lim<<<(B + 255) / 256, 256, 0, s>>>(B, len, t0, nc, ld, lim, err);
 }
 
 void launch_kv_poison(int B, const int32_t* slots, const int32_t* kv_len, int span, const cache_t& c,

@@ -28,7 +28,7 @@ SD_DTYPE_F32, SD_DTYPE_BF16 = 0, 1
 API_SYMBOLS = (
     "sd_last_error", "sd_create", "sd_destroy", "sd_num_weights", "sd_bind_weights", "sd_kv_bytes",
     "sd_bind_kv", "sd_kv_page_bytes", "sd_bind_kv_paged", "sd_drafter_bytes", "sd_drafter_bytes_fmt", "sd_refresh_drafter", "sd_refresh_drafter_fmt",
-    "sd_prefill", "sd_draft", "sd_verify",
+    "sd_prefill", "sd_prefill_ragged", "sd_draft", "sd_verify",
     "sd_accept", "kv_rollback", "sd_ar_step", "sd_sync", "sd_set_debug", "sd_cost_init",
     "sd_cost_times", "sd_toggle", "sd_gamma_init", "sd_gamma_next", "sd_tau_from_alpha",
     "sd_alpha_from_tau", "sd_timing", "sd_timing_read", "sd_dense_gemm_bf16", "sd_accept_noalloc",
@@ -96,6 +96,7 @@ def lib():
             "sd_drafter_bytes_fmt": (_sz, [_P, _i32]),
             "sd_refresh_drafter_fmt": (_i32, [_P, _i32, _P, _sz, _P]),
             "sd_prefill": (_i32, [_P, _i32, _P, _P, _i32, _P]),
+            "sd_prefill_ragged": (_i32, [_P, _i32, _P, _P, _i32, _P, _P]),
             "sd_draft": (_i32, [_P, _i32, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
             "sd_verify": (_i32, [_P, _i32, _P, _P, _P, _i32, _P, _P]),
             "sd_accept": (_i32, [_P, _i32, _P, _P, _P, _P, _P, _i32, _f, Rng, _P, _P, _P, _P]),
@@ -271,6 +272,13 @@ class Engine:
         n = tokens.shape[1]
         _check(lib().sd_prefill(self.h, B, sp, _dev(tokens, "tokens", torch.int32, (B, n), self.device), n,
                                 _stream()))
+
+    def prefill_ragged(self, slots, tokens, lens):
+        """Caches tokens[b, :lens[b]] of each sequence; tokens is [B][ld], lens [B] (device int32)."""
+        B, sp = self._slots(slots)
+        ld = tokens.shape[1]
+        _check(lib().sd_prefill_ragged(self.h, B, sp, _dev(tokens, "tokens", torch.int32, (B, ld), self.device), ld,
+                                       _dev(lens, "lens", torch.int32, (B,), self.device), _stream()))
 
     def draft(self, slots, last_tok, gamma, T, seed, step, draft_tok, q_logits, q_stats):
         B, sp = self._slots(slots)
