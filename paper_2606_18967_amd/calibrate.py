@@ -284,8 +284,8 @@ def main(argv=None):
     ap.add_argument("--model", default="L4_8B", choices=["L4_8B", "L32_8B", "L64_32B", "TINY_BF16"])
     ap.add_argument("--B", default="1,4,16,64,128,256")
     ap.add_argument("--S", default="512,2048,8192")
-    ap.add_argument("--gamma", default="3,7,11")
-    ap.add_argument("--tau", default="2,3,4,5.5,7.5")
+    ap.add_argument("--gamma", default="3,7,11,15")
+    ap.add_argument("--tau", default="2,3,4,5.5,7.5,10,13")
     ap.add_argument("--eps", type=float, default=0.05)
     ap.add_argument("--reps", type=int, default=8)
     ap.add_argument("--out", default="")

@@ -155,12 +155,13 @@ def test_device_range_errors_are_reported():
     eng.close()
 
 
-@pytest.mark.parametrize("M", [65, 130, 190, 200, 300, 320, 384, 600, 640, 700])
+@pytest.mark.parametrize("M", [65, 130, 190, 200, 300, 320, 384, 600, 640, 700, 1000, 1536])
 def test_dense_gemm_verify_rows(M):
     """The bf16 GEMM at the verify forward's row counts (M > 64: the LDS-tiled
     kernels with 128- to 320-row tiles, ragged last tiles included; 300, 320,
-    600 and 640 rows take the DMA-fed 320-row tiles, 128 columns wide at this
-    N) against torch in fp32 on the same bf16 inputs."""
+    600, 640, 700, 1000 and 1536 rows take the DMA-fed 320-row tiles, one to
+    five of them, 128 columns wide at this N) against torch in fp32 on the
+    same bf16 inputs."""
     say("verify-rows gemm", M)
     g = torch.Generator(device="cuda").manual_seed(M)
     N, K = 24576, 1024
@@ -199,11 +200,12 @@ WIDE_FFN = dict(name="wide-ffn-bf16", n_layers=1, hidden=256, n_q=4, n_kv=2, hea
 
 @pytest.mark.parametrize("fmt", ["w4", "w4a", "w8"])
 @pytest.mark.parametrize("B,cfg", [(3, SMALL_BF16), (16, SMALL_BF16), (64, SMALL_BF16), (20, WIDE_FFN),
-                                   (64, WIDE_FFN)], ids=["3", "16", "64", "wide-20", "wide-64"])
+                                   (64, WIDE_FFN), (128, WIDE_FFN)], ids=["3", "16", "64", "wide-20", "wide-64",
+                                                                          "wide-128"])
 def test_fused_swiglu_equals_separate_kernel(B, cfg, fmt):
     """SwiGLU in the gate/up GEMM's epilogue (the int4 drafter GEMM with one or
-    two 32-row tiles where it runs unsplit; the tiled bf16 verify GEMM at 80
-    and 320 rows) gives the same SD step, bit for bit, as the gate/up GEMM
+    two 32-row tiles where it runs unsplit; the tiled bf16 verify GEMM at 80,
+    320 and 640 rows) gives the same SD step, bit for bit, as the gate/up GEMM
     followed by the SwiGLU kernel: same fp32 sums, same SiLU."""
     say("fused swiglu", B, cfg["name"], fmt)
     gamma, T, seed, S = 4, 1.0, 31, 48
@@ -229,12 +231,13 @@ def test_fused_swiglu_equals_separate_kernel(B, cfg, fmt):
 
 
 @pytest.mark.parametrize("fmt", ["w4", "w8"])
-@pytest.mark.parametrize("B", [52, 64])
+@pytest.mark.parametrize("B", [52, 64, 128, 160])
 def test_dma_fed_tiles_equal_register_staged_tiles(B, fmt):
     """The verify forward's 320-row GEMM tiles loaded into LDS by DMA (all four
     projections, SwiGLU fused, and the LM head) give the same SD step, bit
     for bit, as the register-staged tiles: the same MFMA operands in the same
-    k order.  B = 52 leaves 60 of the 320 rows empty."""
+    k order.  B = 52 leaves 60 of the 320 rows empty; B = 128 and 160 (640
+    and 800 rows) run two and three m-tiles, the last one half empty at 160."""
     say("dma-fed tiles", B, fmt)
     cfg = SMALL_BF16
     gamma, T, seed, S = 4, 1.0, 37, 40
