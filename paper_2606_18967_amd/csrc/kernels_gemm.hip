@@ -741,20 +741,12 @@ static int tiled_mtw(int M)
 }
 
 // The height every form of the tiled GEMM takes.  Past 320 rows the 320-row
-// tiles are the fastest per weight byte (fed by LDS DMA; at 8192^3 they run
-// at 894 TFLOP/s against 537 for 256-row register-staged tiles, and at
-// M = 1536 at 787 against 588), so they are taken unless they pad more than a
-// quarter beyond the tightest height.
-static int gemm_mtw(int M)
-{
-    const int t = tiled_mtw(M);
-    if (M > 320 && t != 10) {
-        const long r10 = (long)((M + 319) / 320) * 320;
-        const long rt = (long)((M + 32 * t - 1) / (32 * t)) * 32 * t;
-        if (4 * r10 <= 5 * rt) return 10;
-    }
-    return t;
-}
+// tiles fed by LDS DMA win even where they pad: fewer passes over the weights
+// at a higher rate per pass (measured at N = 28672, K = 4096: 142 against
+// 158 us at M = 330, 144 against 228 us at M = 448; 894 against 537 TFLOP/s
+// at 8192^3).  Up to 320 rows the tightest height stays (at 96-256 rows the
+// shorter tiles are faster).
+static int gemm_mtw(int M) { return M > 320 ? 10 : tiled_mtw(M); }
 
 #ifndef TILED_SPLIT_TARGET
 #define TILED_SPLIT_TARGET 192

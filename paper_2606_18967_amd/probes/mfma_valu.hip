@@ -36,7 +36,7 @@ constexpr int CUS = 256;    // one work-group per CU, 4 * waves-per-SIMD waves e
 
 // ---------------------------------------------------------------- 1. shape rates
 // KIND 0: 32x32x16 f16, 1: 32x32x16 bf16, 2: 16x16x32 f16, 3: 16x16x32 bf16;
-// each iteration does 4 x 32768 FLOP (four 32x32x16 or sixteen 16x16x32)
+// each iteration does 4 x 32768 FLOP (four 32x32x16 or eight 16x16x32)
 template <int KIND>
 __global__ void k_rate(float* out, int iters)
 {
@@ -64,7 +64,7 @@ __global__ void k_rate(float* out, int iters)
             x3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c, d, x3, 0, 0, 0);
         } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < 2; ++r) {
                 if constexpr (KIND == 2) {
                     y0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, y0, 0, 0, 0);
                     y1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, y1, 0, 0, 0);
