@@ -5,8 +5,9 @@
     context, gamma = 4: the launch configuration bench.py times with this
     model.  Two SD steps, then four AR steps.
   - The 32B shape (hidden 5120, 40 query / 8 KV heads x 128 -- five query
-    heads per KV head --, FFN 27648, vocab 152064) at two layers, B = 64, 512
-    positions of context: the per-layer shapes of the 64-layer workload.
+    heads per KV head --, FFN 27648, vocab 152064) at two layers, B = 64 and
+    B = 128, 512 positions of context: the per-layer shapes of the 64-layer
+    workload (B = 128 runs every GEMM over two m-tiles).
 
 For every one of the 64 sequences, every decision is checked on the device's
 own logits (oracle.parity): the 256 draft draws and their q row statistics
@@ -123,4 +124,15 @@ def test_32b_shaped_two_layer_full_size_matches_oracle():
     cfg = dict(synth.L64_32B, n_layers=2, name="32B-shape-2L")
     t = _full_size(cfg, 64, 512, 4, 1.0, 11, 1, [5, 30, 33, 62], sd_steps=1, ar_steps=4)
     assert t["draw_rows"] >= 256 + 256 and t["logit_checks"] == 4 + 4 * 4
+    assert t["exempt"] <= 1
+
+
+def test_32b_shaped_two_layer_full_size_b128_matches_oracle():
+    """B = 128 (the B = 128, 4096-position form of the 64-layer workload): the
+    verify GEMMs run two 320-row DMA m-tiles (640 rows), the drafter GEMMs two
+    64-row m-tiles, and the AR step's streaming GEMM two m-tiles; sampled
+    sequences sit in both m-tiles of each."""
+    cfg = dict(synth.L64_32B, n_layers=2, name="32B-shape-2L")
+    t = _full_size(cfg, 128, 512, 4, 1.0, 12, 1, [0, 63, 64, 100, 127], sd_steps=1, ar_steps=2)
+    assert t["draw_rows"] >= 128 * 4 + 2 * 128 and t["logit_checks"] == 5 + 2 * 5
     assert t["exempt"] <= 1
