@@ -1,8 +1,10 @@
 // kernels_gemm.hip -- the bf16 projections: C[M][N] (fp32) = or += A[M][K] W^T.
 //
 // Weights are row-major [N][K] (K contiguous), activations [M][K].
-//   - gemm_stream (M <= 64 per m-tile): weights streamed from HBM into
-//     registers, v_mfma_f32_16x16x32_bf16; see k_gemm_stream.
+//   - gemm_dma64 (M <= 64, N a multiple of 256): 64-row tiles with both
+//     operands brought into LDS by DMA through a three-stage ring; see
+//     k_gemm_dma64.  gemm_stream (M <= 64, other N): weights streamed from
+//     HBM into registers, v_mfma_f32_16x16x32_bf16; see k_gemm_stream.
 //   - gemm_tiled (M > 64, the verify forward): both operands through LDS.
 //   - gemm_f32 / gemm_q4_f32: plain VALU versions for fp32 models (the int4
 //     one reads the packed layout of kernels_q4.hip).
@@ -642,6 +644,113 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
         }
 }
 
+// ------------------------------------------------------------------ 64-row tiles fed by LDS DMA
+// The decode-shaped GEMM (M <= 64: the AR step's projections, the draft LM
+// head) as a 64 x 256 tile of the DMA-fed kernel above: eight waves, each a
+// 32 x 64 block of v_mfma_f32_32x32x16_bf16, operands brought into LDS by
+// global_load_lds_dwordx4 in whole 128-byte lines.  At 64 rows the tile
+// computes little per stage, so the ring is three stages deep (two in
+// flight while one is multiplied; 120 KB of LDS).  Streaming the weights
+// straight into registers in the MFMA layout (k_gemm_stream) reads 64 bytes
+// from each of 16 rows 10 KB apart per instruction and reaches 2.3-4.3 TB/s
+// at the 32B shape's projections; this tile reaches 3.7-6.0 TB/s (gate/up
+// 137 -> 95 us, down 85 -> 49 us, LM head 368 -> 309 us at M = 64).  Rows past
+// M repeat row M - 1 (never stored); split-K partials as in k_gemm_dma.
+constexpr int D64R = 3;                                 // LDS ring stages
+
+__global__ void __launch_bounds__(512) k_gemm_dma64(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+                                                    float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
+                                                    int ldc, int mode, int S, int total)
+{
+    constexpr int BM = 64, BN = 256, NWAVE = 8, NB = D64R;
+    constexpr int NA = BM / 8, NI = NA + BN / 8;            // 1 KB pieces (8 rows of 128 B) per stage
+    constexpr int STG = (BM + BN) * DRB;
+    constexpr int CNT = NI / NWAVE;
+    static_assert(NI % NWAVE == 0 && NB == 3, "five pieces per wave, waits written for three stages");
+    __shared__ __attribute__((aligned(1024))) uint8_t sm[NB * STG];
+    const uint32_t sbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)sm;
+    const int per_xcd = gridDim.x >> 3;                     // gridDim.x is a multiple of 8
+    const int w = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (w >= total) return;
+    const int s = w % S, nt = w / S;
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wv >> 2, wn = wv & 3;
+    const int n0 = nt * BN;
+    const int Ks = K / DBK / S, k0 = s * Ks;
+
+    const uint16_t* src[CNT];
+    uint32_t dst[CNT];
+#pragma unroll
+    for (int q = 0; q < CNT; ++q) {
+        const int t = wv + q * NWAVE, rl = lane >> 3, pos = lane & 7;
+        if (t < NA) {
+            const int row = 8 * t + rl;
+            src[q] = A + (size_t)min(row, M - 1) * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
+            dst[q] = t * 1024;
+        } else {
+            const int row = 8 * (t - NA) + rl;
+            src[q] = W + (size_t)(n0 + row) * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
+            dst[q] = BM * DRB + (t - NA) * 1024;
+        }
+    }
+    auto issue = [&](int buf, int kb) {
+#pragma unroll
+        for (int q = 0; q < CNT; ++q) {
+            if (wv + q * NWAVE < NA) lds_dma16(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+            else lds_dma16_nt(src[q] + (size_t)kb * DBK, sbase + buf * STG + dst[q]);
+        }
+    };
+
+    floatx16 acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+
+    issue(0, 0);
+    if (Ks > 1) issue(1, 1);
+    for (int kb = 0; kb < Ks; ++kb) {
+        // this wave's pieces of stage kb are in once those of the (at most one) later stage are all that is outstanding
+        if (kb + 1 < Ks) wait_vmcnt<CNT>();
+        else wait_vmcnt<0>();
+        lds_barrier();                      // everyone's are, and stage kb - 1 is no longer read
+        if (kb + 2 < Ks) issue((kb + 2) % NB, kb + 2);
+        const uint8_t* sa = sm + (kb % NB) * STG;
+        const uint8_t* sw = sa + BM * DRB;
+#pragma unroll
+        for (int ks = 0; ks < DBK / 16; ++ks) {
+            const int c = 2 * ks + (lane >> 5);
+            const int ra = wm * 32 + (lane & 31);
+            const u32x4 af = *(const u32x4*)(sa + ra * DRB + ((c ^ dma_sw(ra)) << 4));
+            u32x4 bw[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int r = wn * 64 + 32 * j + (lane & 31);
+                bw[j] = *(const u32x4*)(sw + r * DRB + ((c ^ dma_sw(r)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af),
+                                                                 __builtin_bit_cast(bf16x8, bw[j]), acc[j], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 64 + 32 * j + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row >= M) continue;
+            if (S == 1) {
+                float* cp = C + (size_t)row * ldc + col;
+                *cp = mode == GEMM_ADD ? *cp + acc[j][r] : acc[j][r];
+            } else {
+                P[((size_t)s * M + row) * N + col] = acc[j][r];
+            }
+        }
+    }
+}
+
 // C[m][n] (+)= sum_s P[s][m][n]
 __global__ void __launch_bounds__(256) k_splitk_reduce(const float* __restrict__ P, float* __restrict__ C, int M, int N,
                                                        int ldc, int S, int mode)
@@ -793,10 +902,36 @@ static void dma_plan(int M, int N, int K, int* wn, int* S)
     }
 }
 
+// the 64-row DMA tiles: N a multiple of 256, K of 64 (at least two stages)
+static bool use_dma64(int M, int N, int K) { return M <= 64 && N % 256 == 0 && K % DBK == 0 && K >= 2 * DBK; }
+
+#ifndef DMA64_SPLIT_TARGET
+#define DMA64_SPLIT_TARGET 192
+#endif
+
+// split count of the 64-row tiles: the smallest divisor S of the K / 64
+// stages (at least two stages per split, at most 32 splits) giving
+// DMA64_SPLIT_TARGET work-groups, else the largest such S
+static int dma64_split(int N, int K)
+{
+    const int tiles = N / 256, KB = K / DBK;
+    int S = 1;
+    for (int s = 1; s <= 32 && 2 * s <= KB; ++s) {
+        if (KB % s) continue;
+        S = s;
+        if (tiles * s >= DMA64_SPLIT_TARGET) break;
+    }
+    return S;
+}
+
 size_t gemm_part_floats(int M, int N, int K)
 {
     int nbw, S;
     gemm_plan(M, N, K, &nbw, &S);
+    if (use_dma64(M, N, K)) {
+        const int S64 = dma64_split(N, K);
+        S = S64 > S ? S64 : S;
+    }
     if (use_tiled(M, N, K)) {
         int mtw, St;
         tiled_plan(M, N, K, &mtw, &St);
@@ -854,6 +989,17 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
             case 5: k_gemm_tiled<5><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total); break;
             default: k_gemm_t32<4, false><<<grid, 256, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, mtiles, total, nullptr, 0); break;
         }
+        if (S > 1 && !defer_reduce) {
+            size_t MN = (size_t)M * N;
+            k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
+        }
+        return S;
+    }
+    if (use_dma64(M, N, K)) {
+        int S = dma64_split(N, K);
+        if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
+        const int total = N / 256 * S;
+        k_gemm_dma64<<<dim3((total + 7) / 8 * 8), 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, total);
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);

@@ -175,6 +175,26 @@ def test_dense_gemm_verify_rows(M):
     assert err <= 1e-4 * ref.abs().max().item(), err
 
 
+@pytest.mark.parametrize("N", [24576, 4224])
+@pytest.mark.parametrize("M", [1, 5, 16, 33, 64])
+def test_dense_gemm_decode_rows(M, N):
+    """The bf16 GEMM at the AR step's and draft LM head's row counts (M <= 64):
+    the DMA-fed 64-row tiles where N is a multiple of 256 (rows past M repeat
+    the last row and are never stored), the register-streaming kernel
+    otherwise (N = 4224), against torch in fp32 on the same bf16 inputs."""
+    say("decode-rows gemm", M, N)
+    g = torch.Generator(device="cuda").manual_seed(1000 + M)
+    K = 1024
+    A = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    W = torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)
+    out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    sdrl.dense_gemm_bf16(A, W, out)
+    ref = A.float() @ W.float().t()
+    torch.cuda.synchronize()
+    err = (out - ref).abs().max().item()
+    assert err <= 1e-4 * ref.abs().max().item(), err
+
+
 @pytest.mark.parametrize("M", [300, 320])
 def test_dense_gemm_wide_dma_tiles(M):
     """N with at least 256 tiles of 256 columns: the DMA-fed 320 x 256 tiles
