@@ -655,12 +655,17 @@ __global__ void __launch_bounds__(128 * WN) k_gemm_dma(const uint16_t* __restric
 // from each of 16 rows 10 KB apart per instruction and reaches 2.3-4.3 TB/s
 // at the 32B shape's projections; this tile reaches 3.7-6.0 TB/s (gate/up
 // 137 -> 95 us, down 85 -> 49 us, LM head 368 -> 309 us at M = 64).  Rows past
-// M repeat row M - 1 (never stored); split-K partials as in k_gemm_dma.
+// M repeat row M - 1 (never stored); split-K partials as in k_gemm_dma.  SW:
+// the SwiGLU epilogue of k_gemm_dma (a tile of 128 features; wave column
+// wn's two 32-column blocks are the gate and the up rows of the same 32
+// features), used where the gate/up projection runs unsplit.
 constexpr int D64R = 3;                                 // LDS ring stages
 
+template <bool SW>
 __global__ void __launch_bounds__(512) k_gemm_dma64(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
                                                     float* __restrict__ C, float* __restrict__ P, int M, int N, int K,
-                                                    int ldc, int mode, int S, int total)
+                                                    int ldc, int mode, int S, int total, void* __restrict__ out,
+                                                    int out_t)
 {
     constexpr int BM = 64, BN = 256, NWAVE = 8, NB = D64R;
     constexpr int NA = BM / 8, NI = NA + BN / 8;            // 1 KB pieces (8 rows of 128 B) per stage
@@ -689,7 +694,12 @@ __global__ void __launch_bounds__(512) k_gemm_dma64(const uint16_t* __restrict__
             dst[q] = t * 1024;
         } else {
             const int row = 8 * (t - NA) + rl;
-            src[q] = W + (size_t)(n0 + row) * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
+            int wrow = n0 + row;
+            if constexpr (SW) {
+                const int f = nt * (BN / 2) + (row >> 6) * 32 + (row & 31);   // wave column row/64, block (row/32)%2
+                wrow = ((row >> 5) & 1) ? N / 2 + f : f;
+            }
+            src[q] = W + (size_t)wrow * K + (size_t)k0 * DBK + 8 * (pos ^ dma_sw(row));
             dst[q] = BM * DRB + (t - NA) * 1024;
         }
     }
@@ -733,6 +743,21 @@ __global__ void __launch_bounds__(512) k_gemm_dma64(const uint16_t* __restrict__
                 acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af),
                                                                  __builtin_bit_cast(bf16x8, bw[j]), acc[j], 0, 0, 0);
         }
+    }
+    if constexpr (SW) {
+        const int F = N / 2, feat = nt * (BN / 2) + wn * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row >= M) continue;
+            const float g = acc[0][r], u = acc[1][r];
+            const float v = g / (1.f + __expf(-g)) * u;
+            const size_t oi = (size_t)row * F + feat;
+            if (out_t == ACT_F16) store_act<_Float16>(out, oi, v);
+            else if (out_t == ACT_BF16) store_act<uint16_t>(out, oi, v);
+            else store_act<float>(out, oi, v);
+        }
+        return;
     }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -999,7 +1024,8 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
         int S = dma64_split(N, K);
         if (S > 1 && (size_t)S * M * N > part_cap) S = 1;   // workspace too small: no split
         const int total = N / 256 * S;
-        k_gemm_dma64<<<dim3((total + 7) / 8 * 8), 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, total);
+        k_gemm_dma64<false><<<dim3((total + 7) / 8 * 8), 512, 0, s>>>(A, W, C, part, M, N, K, ldc, mode, S, total,
+                                                                       nullptr, 0);
         if (S > 1 && !defer_reduce) {
             size_t MN = (size_t)M * N;
             k_splitk_reduce<<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(part, C, M, N, ldc, S, mode);
@@ -1031,6 +1057,14 @@ int launch_gemm_bf16(const uint16_t* A, const uint16_t* W, float* C, float* part
 int launch_gemm_bf16_swiglu(const uint16_t* A, const uint16_t* W, void* out, act_t out_t, int M, int F, int K,
                             hipStream_t s, bool lds_dma)
 {
+    if (use_dma64(M, 2 * F, K) && F % 128 == 0) {
+        // 64-row tiles: fused only where the plain projection runs unsplit
+        if (dma64_split(2 * F, K) != 1) return 0;
+        const int total = F / 128;
+        k_gemm_dma64<true><<<dim3((total + 7) / 8 * 8), 512, 0, s>>>(A, W, nullptr, nullptr, M, 2 * F, K, 0, 0, 1,
+                                                                      total, out, (int)out_t);
+        return 1;
+    }
     if (!use_tiled(M, 2 * F, K) || F % 64) return 0;
     const int mtw = gemm_mtw(M);
     if (mtw == 5) return 0;                              // the 16x16x32 kernel has no SwiGLU epilogue

@@ -250,6 +250,33 @@ def test_fused_swiglu_equals_separate_kernel(B, cfg, fmt):
     eng.close()
 
 
+@pytest.mark.parametrize("B", [5, 64])
+def test_fused_swiglu_equals_separate_kernel_ar_step(B):
+    """The AR step's gate/up projection at M <= 64 (the 64-row DMA tiles,
+    unsplit at this FFN width) with SwiGLU in its epilogue gives the same
+    logits, token and KV, bit for bit, as the projection followed by the
+    SwiGLU kernel."""
+    say("fused swiglu, AR step", B)
+    cfg, T, seed, S = WIDE_FFN, 1.0, 41, 32
+    W = [w.cuda() for w in synth.make_weights(cfg, 43, "cpu")]
+    eng, k, v, kv_len = make_engine(cfg, W, B, S + 4, 4)
+    synth.fill_kv_context(k, v, S, 47)
+    slots = torch.arange(B, dtype=torch.int32, device="cuda")
+    last = synth.make_tokens(B, 1, cfg["vocab"], 53)[:, 0].cuda().contiguous()
+    outs = []
+    for unfused in (False, True):
+        eng.set_debug(False, unfused_swiglu=unfused)
+        kv_len.fill_(S)
+        tok = torch.zeros(B, dtype=torch.int32, device="cuda")
+        pl = torch.zeros((B, cfg["vocab"]), dtype=torch.float32, device="cuda")
+        eng.ar_step(slots, last, T, seed, 1, tok, pl)
+        eng.sync()
+        outs.append([t.cpu() for t in (pl, tok, k[:, :, :, S].contiguous(), v[:, :, :, S].contiguous())])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    eng.close()
+
+
 @pytest.mark.parametrize("fmt", ["w4", "w8"])
 @pytest.mark.parametrize("B", [52, 64, 128, 160])
 def test_dma_fed_tiles_equal_register_staged_tiles(B, fmt):
