@@ -120,7 +120,7 @@ KERNEL_OF_CLASS = {
     "int4_proj": "k_gemm_q4<2, 0, false> (qkv, o, down; gate/up runs unsplit as the SwiGLU variant <2, 0, true> "
                  "where N allows)",
     "bf16_proj": "k_gemm_dma<4, false> (qkv, o, down; gate/up runs as the SwiGLU variant <4, true> where N allows)",
-    "lm_head": "k_gemm_dma64 (draft rows), k_gemm_dma<4, false> (verify rows)",
+    "lm_head": "k_gemm_dma64<false> (draft rows), k_gemm_dma<4, false> (verify rows)",
 }
 # the counter ingest keeps, per class, only the dispatches of its kernel
 # launched by that class (work-group counts tell the verify LM head, 594
