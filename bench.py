@@ -245,8 +245,9 @@ def main():
         ingest_pmc(*args.ingest_pmc, os.path.join(ROOT, "profiles", "traffic.json"))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (each GPU would run its own "
-              "sequences independently; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the SD step has no multi-GPU path (data parallelism gives each GPU "
+              "its own sequences, target, drafter and KV cache, with nothing exchanged per step). "
+              "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
