@@ -195,6 +195,22 @@ def test_dense_gemm_decode_rows(M, N):
     assert err <= 1e-4 * ref.abs().max().item(), err
 
 
+@pytest.mark.parametrize("M,N,K", [(1, 256, 128), (64, 512, 384), (17, 768, 640), (64, 256, 27648)])
+def test_dense_gemm_decode_rows_edges(M, N, K):
+    """The 64-row DMA tiles at their edges: the fewest stages (K = 128), one
+    256-column tile, six and ten stages, and one tile over a long K."""
+    say("decode-rows gemm edges", M, N, K)
+    g = torch.Generator(device="cuda").manual_seed(M * 7 + N + K)
+    A = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    W = torch.randn((N, K), generator=g, device="cuda").to(torch.bfloat16)
+    out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    sdrl.dense_gemm_bf16(A, W, out)
+    ref = A.float() @ W.float().t()
+    torch.cuda.synchronize()
+    err = (out - ref).abs().max().item()
+    assert err <= 1e-4 * ref.abs().max().item(), err
+
+
 @pytest.mark.parametrize("M", [300, 320])
 def test_dense_gemm_wide_dma_tiles(M):
     """N with at least 256 tiles of 256 columns: the DMA-fed 320 x 256 tiles
