@@ -432,16 +432,18 @@ def main(argv=None):
     lengths_fn = lambda t: response_lengths(a.B, a.median, a.sigma, a.lmin, a.lmax, a.seed * 1000 + t)
     # one untimed rollout to load every kernel
     ro.run("sd", GAMMA_SET[0], float(GAMMA_SET[0]), cost, EPS, np.minimum(lengths_fn(0), 64), 99, keep_trace=False)
+    def run_and_report(p, g, tp, L, t):
+        r = ro.run(p, g, tp, cost, EPS, L, t)[0]
+        # one line per training step as soon as it ends (a policy's steps can take minutes in all)
+        log(f"{p:9s} step {r.step}: gamma {r.gamma:2d}  tau_prev {r.tau_prev:5.2f}  tau "
+            f"{'  -  ' if r.tau is None else f'{r.tau:5.2f}'}  makespan {r.makespan_s:7.3f} s  "
+            f"AR iters {r.ar_iters:5d}  SD iters {r.sd_iters:5d}  SD on at B={r.switch_B}  prep {r.prep_ms:.1f} ms"
+            f"  graphs {r.graphs} ({r.capture_s:.2f} s to capture)")
+        return r
+
     results = {}
     for pol in a.policies.split(","):
-        rs = train(lambda p, g, tp, L, t: ro.run(p, g, tp, cost, EPS, L, t)[0], pol, a.steps, lengths_fn,
-                   tau_carry=a.tau_carry)
-        results[pol] = rs
-        for r in rs:
-            log(f"{pol:9s} step {r.step}: gamma {r.gamma:2d}  tau_prev {r.tau_prev:5.2f}  tau "
-                f"{'  -  ' if r.tau is None else f'{r.tau:5.2f}'}  makespan {r.makespan_s:7.3f} s  "
-                f"AR iters {r.ar_iters:5d}  SD iters {r.sd_iters:5d}  SD on at B={r.switch_B}  prep {r.prep_ms:.1f} ms"
-                f"  graphs {r.graphs} ({r.capture_s:.2f} s to capture)")
+        results[pol] = train(run_and_report, pol, a.steps, lengths_fn, tau_carry=a.tau_carry)
     ro.close()
     L0 = lengths_fn(0)
     summary = dict(model=cfg["name"], drafter=a.drafter, B=a.B, prompt=a.prompt, tau_carry=a.tau_carry,
