@@ -139,10 +139,11 @@ def algorithmic_per_launch(cfg, B, gamma, ctx, drafter="w4"):
     what the kernels happen to transfer."""
     H, V, d, nkv, nq, F = (cfg[x] for x in ("hidden", "vocab", "head_dim", "n_kv", "n_q", "ffn"))
     kv_pos = nkv * d * 2 * 2                 # K and V bytes per cached position per layer (bf16)
-    q_row = nq * d * 4                       # fp32 rotated queries per token
-    # draft j (1..gamma) attends kv_len + j positions; verify attends kv_len + gamma + 1 once for all rows
-    attn_d = B * kv_pos * (ctx + (gamma + 1) / 2) + B * q_row
-    attn_v = B * kv_pos * (ctx + gamma + 1) + B * (gamma + 1) * q_row
+    qkv_row = (nq + 2 * nkv) * d * 4         # fp32 QKV projection row per token (RoPE is part of the attention)
+    # draft j (1..gamma) attends kv_len + j positions; verify attends kv_len + gamma + 1 once for all rows;
+    # each token's projection row is read and its new K/V row written
+    attn_d = B * kv_pos * (ctx + (gamma + 1) / 2) + B * (qkv_row + kv_pos)
+    attn_v = B * kv_pos * (ctx + gamma + 1) + B * (gamma + 1) * (qkv_row + kv_pos)
     w_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F          # projection weights per layer
     q4 = w_layer * DRAFTER_BYTES_PER_WEIGHT[drafter] / 4                # mean drafter launch (4 per layer)
     rows_v = B * (gamma + 1)

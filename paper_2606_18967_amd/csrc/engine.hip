@@ -481,11 +481,16 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
       launch_embed_rmsnorm(r, tokA, sA, tokB, sB, e->w[0], e->f32, c.hidden, c.vocab, e->h, W(e, 0, 0), c.rms_eps, e->a, at, s); }
     for (int l = 0; l < c.n_layers; ++l) {
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_QKV, e->a, e->qkv, R, qkvN, GEMM_STORE, s); }
-        { tscope t(e, T_MISC, s); launch_rope_kv(r, e->qkv, e->gpart, S, e->rope, c.n_q, kv, l, e->qrot, s); }
-        if (!logits && l == c.n_layers - 1) break;      // the rest of the last layer only feeds the logits
+        if (!logits && l == c.n_layers - 1) {
+            // the rest of the last layer only feeds the logits: the new K/V rows alone
+            tscope t(e, T_MISC, s);
+            launch_rope_kv(r, e->qkv, e->gpart, S, e->rope, c.n_q, kv, l, e->qrot, s);
+            break;
+        }
         attn_split sp;
-        { kscope t(e, n == 1 ? T_ATTN_D : T_ATTN_V);
-          sp = launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s, t.start, t.stop); }
+        { kscope t(e, n == 1 ? T_ATTN_D : T_ATTN_V);      // RoPE and the new K/V rows are part of the attention
+          sp = launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s, t.start, t.stop,
+                                qkv_src{e->qkv, e->gpart, S, e->rope}); }
         if (!sp.done) { tscope t(e, T_MISC, s); launch_attention_combine(r, c.n_q, c.head_dim, e->att_part, sp, e->att, at, s); }
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
         { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }

@@ -127,6 +127,18 @@ __device__ __forceinline__ float sum_parts(const float* src, const float* P, int
     return add_splits(0.f, P, S, RN, idx);
 }
 
+// rotate-half RoPE of the column pair (a, c) = (x_k, x_{k + d/2}) with (cos, sin) = cs
+__device__ __forceinline__ float2 rope_rot(float a, float c, float2 cs)
+{
+    return make_float2(a * cs.x - c * cs.y, a * cs.y + c * cs.x);
+}
+
+// element offset of (layer, KV head) inside a cache page (kv_geom)
+__device__ __forceinline__ long long hbase_of(const kv_geom& g, int layer, int kvh)
+{
+    return (long long)layer * g.LS + (long long)kvh * g.HS;
+}
+
 // ------------------------------------------------------------------ rope + kv write
 // qkv row = [q (n_q*d) | k (n_kv*d) | v (n_kv*d)], fp32: n_q + 2 n_kv head
 // units of d columns.  RoPE rotate-half with the (cos, sin) table
@@ -169,8 +181,8 @@ __global__ void __launch_bounds__(256) k_rope_kv(rows_t r, const float* qkv, con
         const size_t c0 = base_idx + (size_t)u * d + k;
         const float a = sum_parts(qkv, P, S, RN, c0), c = sum_parts(qkv, P, S, RN, c0 + hd);
         if (u < n_q + n_kv) {
-            const float2 cs = rp[k];
-            const float x0 = a * cs.x - c * cs.y, x1 = a * cs.y + c * cs.x;
+            const float2 rot = rope_rot(a, c, rp[k]);
+            const float x0 = rot.x, x1 = rot.y;
             if (u < n_q) {
                 qo[(size_t)u * d + k] = x0;
                 qo[(size_t)u * d + k + hd] = x1;
@@ -354,10 +366,18 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 
 // two waves per SIMD where the registers allow it without spills (one query
 // tile; two tiles with a single K/V register set); three or four tiles keep one
+//
+// With the QKV projection's output given (qs.rope set, qkv_src in kernels.h)
+// the kernel also does k_rope_kv's work for its KV head: it writes the new
+// K (rotated) and V rows of its context range to the cache before its waves
+// read them (each work-group of the head covering new positions writes those
+// it reads; query-row slices of one chunk write the same values), and it
+// forms its rotated query rows from the projection's output instead of
+// reading q.  The error flags k_rope_kv raises are raised here then.
 template <int D, int MQ, bool PAGED>
 __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
                                                    const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch,
-                                                   void* out, int out_t)
+                                                   void* out, int out_t, qkv_src qs)
 {
     constexpr int KS = D / 32;      // k-steps over the head dim
     constexpr int NBD = D / 16;     // 16-wide blocks of the head dim
@@ -371,7 +391,9 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     // wave-uniform by construction; readfirstlane lets the compiler keep them
     // (and the buffer resources built from them) in scalar registers
     const int slot = __builtin_amdgcn_readfirstlane(r.slots[b]);
-    if (slot < 0 || slot >= r.max_slots) {         // flagged by k_rope_kv; a direct output is zeroed
+    const bool fused = qs.rope != nullptr;
+    if (slot < 0 || slot >= r.max_slots) {         // flagged (by k_rope_kv unless fused); a direct output is zeroed
+        if (fused && c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0) flag_error(r.err, ERR_SLOT);
         const int G = n_q / n_kv;
         for (int idx = threadIdx.x; out && idx < 16 * MQ * D; idx += 256) {
             const int qrow = z * 16 * MQ + idx / D, d = idx % D;
@@ -387,6 +409,11 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     const int basepos = __builtin_amdgcn_readfirstlane(r.kv_len[slot]) + r.off;
     int ctx = basepos + r.n;
     if (ctx > r.max_ctx) ctx = r.max_ctx;
+    // rows (b, i >= nlive) are padding: neither cached nor flagged
+    const int nlive = r.lim ? min(r.n, max(__builtin_amdgcn_readfirstlane(r.lim[b]), 0)) : r.n;
+    if (fused && c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0 && nlive > 0 &&
+        (basepos < 0 || basepos + nlive > r.max_ctx))
+        flag_error(r.err, ERR_CTX);                 // a live row's position outside [0, max_ctx)
     // the sequence's ceil(ctx / ch) chunks (the count k_attn_combine reads)
     // split its context evenly, in multiples of 32 positions
     const int nch = (ctx + ch - 1) / ch;
@@ -398,14 +425,17 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     const int cq = lane >> 4, lr = lane & 15;
     const int G = n_q / n_kv, QR = G * r.n;
     const int qbase = z * 16 * MQ;
+    const int units = n_q + 2 * n_kv;                          // head units of a projection row
+    const size_t RN = (size_t)r.B * r.n * units * D;           // elements of one split
+
+    const float qscale = 1.4426950408889634f * rsqrtf((float)D);
 
     // Q^T fragments (B operand of S^T = K Q^T), filled after the first K/V
     // loads are issued so that the two memory round trips overlap
-    const float qscale = 1.4426950408889634f * rsqrtf((float)D);
     bf16x8 qf[MQ][KS];
     int lim[MQ];
 
-    const long long hbase = layer * kg.LS + kvh * kg.HS;      // + page * PS (+ (p % P) * D)
+    const long long hbase = hbase_of(kg, layer, kvh);         // + page * PS (+ (p % P) * D)
     const uint16_t* K = kc + (PAGED ? 0 : slot * kg.PS) + hbase;
     const uint16_t* V = vc + (PAGED ? 0 : slot * kg.PS) + hbase;
     uint16_t* vs = Vs[w];
@@ -548,7 +578,72 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
 
     // two register sets: the next block's K and V load while this one computes
     u32x4 kf0[2][KS], kf1[2][KS], vv0[CPP / 2], vv1[CPP / 2];
-    load_kv(wq0, kf0, vv0);
+    // fused: a wave whose first block holds no new row loads it during the pass below
+    const bool early = fused && wq0 + 32 <= basepos;
+    if (!fused || early) load_kv(wq0, kf0, vv0);
+    // fused: one pass of the work-group over (a) its 16 MQ query rows, rotated,
+    // scaled and rounded to bf16 into LDS (the V tiles' space, unused until the
+    // first block) and (b) its KV head's new rows [n0, p1), K rotated and V,
+    // stored to the cache.  A task is 4 columns and their RoPE partners D/2
+    // further; a thread's task loads go out together, so the pass costs a
+    // memory round trip or two before the K/V stream starts.
+    uint16_t* qst = &Vs[0][0];                                  // [16 MQ][D]
+    static_assert(16 * MQ * D <= 4 * 32 * LDV, "query rows fit the V tiles");
+    if (fused) {
+        constexpr int QG = D / 8;                               // 4-column groups of a half row
+        const int n0 = max(p0, basepos), nkv = max(p1 - n0, 0);
+        const int nq = 16 * MQ * QG, ntask = nq + nkv * 2 * QG;
+        const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        auto sum4 = [&](size_t ci) {
+            return qs.S <= 1 ? *(const float4*)(qs.qkv + ci) : add_splits(z4, qs.P, qs.S, RN, ci);
+        };
+        // columns (a, c) -> (a cos - c sin, a sin + c cos) times scl, for 4 columns
+        auto rot4 = [&](float4 a, float4 c, const float2* rp, float scl, float4& lo, float4& hi) {
+            const float4 c01 = *(const float4*)rp, c23 = *(const float4*)(rp + 2);
+            const float2 r0 = rope_rot(a.x, c.x, make_float2(c01.x, c01.y));
+            const float2 r1 = rope_rot(a.y, c.y, make_float2(c01.z, c01.w));
+            const float2 r2 = rope_rot(a.z, c.z, make_float2(c23.x, c23.y));
+            const float2 r3 = rope_rot(a.w, c.w, make_float2(c23.z, c23.w));
+            lo = make_float4(r0.x * scl, r1.x * scl, r2.x * scl, r3.x * scl);
+            hi = make_float4(r0.y * scl, r1.y * scl, r2.y * scl, r3.y * scl);
+        };
+        auto put4 = [](uint16_t* d, float4 v) { *(uint2*)d = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)); };
+        for (int t = threadIdx.x; t < ntask; t += 256) {
+            if (t < nq) {
+                const int rr = t / QG, gq = t - rr * QG, qrow = qbase + rr;
+                float4 lo = z4, hi = z4;
+                if (qrow < QR) {
+                    const int g = qrow / r.n, i = qrow - g * r.n, pos = basepos + i;
+                    // rows k_rope_kv does not rotate (padding, outside [0, max_ctx)) keep q = 0, as it writes
+                    if (i < nlive && pos >= 0 && pos < r.max_ctx) {
+                        const size_t ci = ((size_t)(b * r.n + i) * units + kvh * G + g) * D + 4 * gq;
+                        rot4(sum4(ci), sum4(ci + D / 2), qs.rope + (size_t)pos * (D / 2) + 4 * gq, qscale, lo, hi);
+                    }
+                }
+                put4(qst + rr * D + 4 * gq, lo);
+                put4(qst + rr * D + D / 2 + 4 * gq, hi);
+            } else {
+                const int tt = t - nq, j = tt / (2 * QG), rem = tt - j * (2 * QG);
+                const bool isv = rem >= QG;
+                const int gq = isv ? rem - QG : rem, i = n0 - basepos + j, pos = basepos + i;
+                if (i >= nlive) continue;                       // padding rows are not cached
+                const long long pg = kv_page(kg, slot, pos / kg.P);
+                if (pg < 0) {
+                    if (gq == 0) flag_error(r.err, ERR_PAGE);
+                    continue;
+                }
+                const size_t ci = ((size_t)(b * r.n + i) * units + n_q + (isv ? n_kv : 0) + kvh) * D + 4 * gq;
+                float4 lo = sum4(ci), hi = sum4(ci + D / 2);
+                if (!isv) rot4(lo, hi, qs.rope + (size_t)pos * (D / 2) + 4 * gq, 1.f, lo, hi);
+                uint16_t* dst = (uint16_t*)(isv ? vc : kc) + pg * kg.PS + hbase_of(kg, layer, kvh) + (long long)(pos % kg.P) * D;
+                put4(dst + 4 * gq, lo);
+                put4(dst + D / 2 + 4 * gq, hi);
+            }
+        }
+        if (nkv > 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the new rows are stored before any wave reads them
+        __syncthreads();                                        // and the query rows are in LDS
+    }
+    if (fused && !early) load_kv(wq0, kf0, vv0);
     // rows past QR read row 0 and are zeroed
 #pragma unroll
     for (int mt = 0; mt < MQ; ++mt) {
@@ -557,6 +652,12 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
         const int qr = live ? qrow : 0;
         const int g = qr / r.n, i = qr - g * r.n;
         lim[mt] = live ? basepos + i : -1;
+        if (fused) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                qf[mt][ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qst + (16 * mt + lr) * D + 8 * (4 * ks + cq)));
+            continue;
+        }
         const float sc = live ? qscale : 0.f;
         const float4* qp = (const float4*)(q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D);
         float4 qv[KS][2];
@@ -572,6 +673,7 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
                                                             pack_bf16x2(c2.x * sc, c2.y * sc), pack_bf16x2(c2.z * sc, c2.w * sc)});
         }
     }
+    if (fused) lds_barrier();                                   // every wave holds its q before the V tiles take the space
 
     if constexpr (MQ == 2) {
         // one register set (246 VGPRs instead of 366): two waves per SIMD, the
@@ -834,12 +936,13 @@ static void launch_ev(F kern, dim3 grid, dim3 block, hipStream_t s, hipEvent_t e
 template <int D, bool PAGED>
 static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const rows_t& r,
                              const float* q, int n_q, const cache_t& c, int layer, float* part, int mch, int ch,
-                             void* out, int out_t)
+                             void* out, int out_t, qkv_src qs)
 {
     const uint16_t* kc = (const uint16_t*)c.k;
     const uint16_t* vc = (const uint16_t*)c.v;
     auto go = [&](auto kern) {
-        launch_ev(kern, grid, dim3(256), s, ev0, ev1, r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t);
+        launch_ev(kern, grid, dim3(256), s, ev0, ev1, r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t,
+                  qs);
     };
     switch (MQ) {
         case 1: go(k_attn_mfma<D, 1, PAGED>); break;
@@ -851,7 +954,8 @@ static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, hipEvent_t ev0, h
 
 template <typename T, int D>
 static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                         int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
+                         int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                         qkv_src qs)
 {
     if constexpr (sizeof(T) == 2) {
         // bf16 cache: MFMA kernel.  max_chunks (the partial buffer's chunk
@@ -871,8 +975,8 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
         dim3 grid(r.B * c.n_kv, mch, zs);
         // one chunk per sequence: the kernel writes the final output itself
         void* o = mch == 1 ? out : nullptr;
-        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t);
-        else attn_mfma_launch<D, false>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t);
+        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t, qs);
+        else attn_mfma_launch<D, false>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t, qs);
         return attn_split{mch, ch, o != nullptr};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
@@ -883,14 +987,20 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
 }
 
 attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
+                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                            qkv_src qs)
 {
-    if (c.head_dim == 128) {
-        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
-        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
+    // the fp32 cache's kernel reads rotated queries: k_rope_kv runs first (into q)
+    if (c.kv_f32 && qs.rope) {
+        launch_rope_kv(r, qs.qkv, qs.P, qs.S, qs.rope, n_q, c, layer, const_cast<float*>(q), s);
+        qs = qkv_src{};
     }
-    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
-    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1);
+    if (c.head_dim == 128) {
+        if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
+        return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
+    }
+    if (c.kv_f32) return attn_t<float, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
+    return attn_t<uint16_t, 64>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
 }
 
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
