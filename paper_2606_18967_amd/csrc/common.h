@@ -127,4 +127,25 @@ __device__ __forceinline__ float4 add_splits(float4 v, const float* P, int S, si
     return v;
 }
 
+// two float4 columns (idx_a, idx_b) summed over S splits, the loads of both in the same batch
+__device__ __forceinline__ void add_splits2(float4& va, float4& vb, const float* P, int S, size_t st, size_t idx_a,
+                                            size_t idx_b)
+{
+    for (int s0 = 0; s0 < S; s0 += 8) {
+        float4 pa[8], pb[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const size_t o = (size_t)min(s0 + u, S - 1) * st;
+            pa[u] = *(const float4*)(P + o + idx_a);
+            pb[u] = *(const float4*)(P + o + idx_b);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s0 + u < S) {
+                va = add4(va, pa[u]);
+                vb = add4(vb, pb[u]);
+            }
+    }
+}
+
 __device__ __forceinline__ void flag_error(uint32_t* err, int kind) { ((volatile uint32_t*)err)[kind] = 1u; }

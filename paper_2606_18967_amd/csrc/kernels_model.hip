@@ -592,10 +592,21 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     if (fused) {
         constexpr int QG = D / 8;                               // 4-column groups of a half row
         const int n0 = max(p0, basepos), nkv = max(p1 - n0, 0);
-        const int nq = 16 * MQ * QG, ntask = nq + nkv * 2 * QG;
+        // tasks: the tile's live query rows, then the new K/V rows, then the
+        // tile's rows past QR (zeros, no loads), so the loading tasks come first
+        const int nlr = max(min(16 * MQ, QR - qbase), 0);
+        const int nlq = nlr * QG, nkt = nkv * 2 * QG, ntask = 16 * MQ * QG + nkt;
         const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        auto sum4 = [&](size_t ci) {
-            return qs.S <= 1 ? *(const float4*)(qs.qkv + ci) : add_splits(z4, qs.P, qs.S, RN, ci);
+        // columns ci and ci + D/2 of the projection output
+        auto sum4x2 = [&](size_t ci, float4& a, float4& c) {
+            a = z4;
+            c = z4;
+            if (qs.S <= 1) {
+                a = *(const float4*)(qs.qkv + ci);
+                c = *(const float4*)(qs.qkv + ci + D / 2);
+            } else {
+                add_splits2(a, c, qs.P, qs.S, RN, ci, ci + D / 2);
+            }
         };
         // columns (a, c) -> (a cos - c sin, a sin + c cos) times scl, for 4 columns
         auto rot4 = [&](float4 a, float4 c, const float2* rp, float scl, float4& lo, float4& hi) {
@@ -609,21 +620,24 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
         };
         auto put4 = [](uint16_t* d, float4 v) { *(uint2*)d = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)); };
         for (int t = threadIdx.x; t < ntask; t += 256) {
-            if (t < nq) {
-                const int rr = t / QG, gq = t - rr * QG, qrow = qbase + rr;
+            if (t < nlq || t >= nlq + nkt) {
+                const int tq = t < nlq ? t : t - nkt;           // query-row task: row rr of the tile
+                const int rr = tq / QG, gq = tq - rr * QG, qrow = qbase + rr;
                 float4 lo = z4, hi = z4;
                 if (qrow < QR) {
                     const int g = qrow / r.n, i = qrow - g * r.n, pos = basepos + i;
                     // rows k_rope_kv does not rotate (padding, outside [0, max_ctx)) keep q = 0, as it writes
                     if (i < nlive && pos >= 0 && pos < r.max_ctx) {
                         const size_t ci = ((size_t)(b * r.n + i) * units + kvh * G + g) * D + 4 * gq;
-                        rot4(sum4(ci), sum4(ci + D / 2), qs.rope + (size_t)pos * (D / 2) + 4 * gq, qscale, lo, hi);
+                        float4 a, c;
+                        sum4x2(ci, a, c);
+                        rot4(a, c, qs.rope + (size_t)pos * (D / 2) + 4 * gq, qscale, lo, hi);
                     }
                 }
                 put4(qst + rr * D + 4 * gq, lo);
                 put4(qst + rr * D + D / 2 + 4 * gq, hi);
             } else {
-                const int tt = t - nq, j = tt / (2 * QG), rem = tt - j * (2 * QG);
+                const int tt = t - nlq, j = tt / (2 * QG), rem = tt - j * (2 * QG);
                 const bool isv = rem >= QG;
                 const int gq = isv ? rem - QG : rem, i = n0 - basepos + j, pos = basepos + i;
                 if (i >= nlive) continue;                       // padding rows are not cached
@@ -633,7 +647,8 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
                     continue;
                 }
                 const size_t ci = ((size_t)(b * r.n + i) * units + n_q + (isv ? n_kv : 0) + kvh) * D + 4 * gq;
-                float4 lo = sum4(ci), hi = sum4(ci + D / 2);
+                float4 lo, hi;
+                sum4x2(ci, lo, hi);
                 if (!isv) rot4(lo, hi, qs.rope + (size_t)pos * (D / 2) + 4 * gq, 1.f, lo, hi);
                 uint16_t* dst = (uint16_t*)(isv ? vc : kc) + pg * kg.PS + hbase_of(kg, layer, kvh) + (long long)(pos % kg.P) * D;
                 put4(dst + 4 * gq, lo);
