@@ -110,9 +110,11 @@ def test_accept_matches_oracle_on_identical_logits(V, mode):
     eng.close()
 
 
-def test_device_range_errors_are_reported():
-    say("range errors")
-    cfg = synth.TINY
+# fp32: k_rope_kv raises the position flags; bf16: the attention kernel does
+# (RoPE and the new K/V rows are part of it there)
+@pytest.mark.parametrize("cfg", [synth.TINY, dict(synth.TINY, dtype="bf16", name="tiny-bf16")], ids=["f32", "bf16"])
+def test_device_range_errors_are_reported(cfg):
+    say("range errors", cfg["name"])
     W = [w.cuda() for w in synth.make_weights(cfg, 2, "cpu")]
     B, gamma = 4, 2
     eng, k, v, kv_len = make_engine(cfg, W, B, 64, gamma)
