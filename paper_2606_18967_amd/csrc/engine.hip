@@ -489,8 +489,8 @@ static void forward(sd_engine e, bool draft, int B, const int32_t* slots, const 
         }
         attn_split sp;
         { kscope t(e, n == 1 ? T_ATTN_D : T_ATTN_V);      // RoPE and the new K/V rows are part of the attention
-          sp = launch_attention(r, e->qrot, c.n_q, kv, l, e->att_part, e->max_chunks, e->att, at, s, t.start, t.stop,
-                                qkv_src{e->qkv, e->gpart, S, e->rope}); }
+          sp = launch_attention(r, qkv_src{e->qkv, e->gpart, S, e->rope}, e->qrot, c.n_q, kv, l, e->att_part,
+                                e->max_chunks, e->att, at, s, t.start, t.stop); }
         if (!sp.done) { tscope t(e, T_MISC, s); launch_attention_combine(r, c.n_q, c.head_dim, e->att_part, sp, e->att, at, s); }
         { tscope t(e, pcls, s); S = proj(e, draft, l, PRJ_O, e->att, e->h, R, c.hidden, GEMM_ADD, s); }
         { tscope t(e, T_MISC, s); launch_add_rmsnorm(e->h, e->gpart, S, R, c.hidden, W(e, l, 3), e->f32, c.rms_eps, e->a, at, s); }

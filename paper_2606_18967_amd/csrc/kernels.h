@@ -58,22 +58,22 @@ void launch_rope_kv(const rows_t& r, const float* qkv, const float* P, int S, co
 // each sequence was a single chunk and the kernel wrote the output itself
 struct attn_split { int chunks, chunk; bool done; };
 // The QKV projection's output as k_rope_kv reads it (qkv, or S > 1 split-K
-// partials P) with the RoPE table.  Given to launch_attention, the RoPE and
-// the cache write of the new rows are part of the attention: with a bf16
-// cache the attention kernel itself rotates its query rows and writes its KV
-// head's new K (rotated) and V rows of its context range before reading them
-// (q is not read); with an fp32 cache k_rope_kv runs first, into q.
+// partials P) with the RoPE table.  The attention applies RoPE and writes the
+// new rows: with a bf16 cache the attention kernel itself rotates its query
+// rows and writes its KV head's new K (rotated) and V rows of its context
+// range before reading them; with an fp32 cache k_rope_kv runs first, writing
+// the rotated queries into q (scratch, [rows][n_q][head_dim] fp32).
 struct qkv_src {
-    const float* qkv = nullptr;
-    const float* P = nullptr;
-    int S = 0;
-    const float2* rope = nullptr;   // NULL: q holds the rotated queries and the cache the new rows
+    const float* qkv;
+    const float* P;
+    int S;
+    const float2* rope;
 };
 // ev0/ev1, when given, are bound to the attention kernel's own dispatch
 // (hipExtLaunchKernelGGL): their elapsed time is the kernel's run time.
-attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
+attn_split launch_attention(const rows_t& r, qkv_src qs, float* q, int n_q, const cache_t& c, int layer, float* part,
                             int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0 = nullptr,
-                            hipEvent_t ev1 = nullptr, qkv_src qs = {});
+                            hipEvent_t ev1 = nullptr);
 void launch_attention_combine(const rows_t& r, int n_q, int head_dim, const float* part, attn_split sp, void* out,
                               act_t out_t, hipStream_t s);
 size_t attention_part_floats(int R, int n_q, int head_dim, int max_chunks);

@@ -367,15 +367,15 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 // two waves per SIMD where the registers allow it without spills (one query
 // tile; two tiles with a single K/V register set); three or four tiles keep one
 //
-// With the QKV projection's output given (qs.rope set, qkv_src in kernels.h)
-// the kernel also does k_rope_kv's work for its KV head: it writes the new
-// K (rotated) and V rows of its context range to the cache before its waves
-// read them (each work-group of the head covering new positions writes those
-// it reads; query-row slices of one chunk write the same values), and it
-// forms its rotated query rows from the projection's output instead of
-// reading q.  The error flags k_rope_kv raises are raised here then.
+// RoPE and the cache write of the new rows are part of the kernel: from the
+// QKV projection's output (qkv_src, kernels.h) each work-group forms its
+// rotated query rows and writes its KV head's new K (rotated) and V rows of
+// its context range to the cache before its waves read them (each
+// work-group of the head covering new positions writes those it reads;
+// query-row slices of one chunk write the same values), and it raises the
+// slot, position and page flags for them.
 template <int D, int MQ, bool PAGED>
-__global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, const float* q, int n_q, int n_kv, const uint16_t* kc,
+__global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, int n_q, int n_kv, const uint16_t* kc,
                                                    const uint16_t* vc, kv_geom kg, int layer, float* part, int max_chunks, int ch,
                                                    void* out, int out_t, qkv_src qs)
 {
@@ -391,9 +391,8 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     // wave-uniform by construction; readfirstlane lets the compiler keep them
     // (and the buffer resources built from them) in scalar registers
     const int slot = __builtin_amdgcn_readfirstlane(r.slots[b]);
-    const bool fused = qs.rope != nullptr;
-    if (slot < 0 || slot >= r.max_slots) {         // flagged (by k_rope_kv unless fused); a direct output is zeroed
-        if (fused && c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0) flag_error(r.err, ERR_SLOT);
+    if (slot < 0 || slot >= r.max_slots) {         // flagged once per sequence; a direct output is zeroed
+        if (c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0) flag_error(r.err, ERR_SLOT);
         const int G = n_q / n_kv;
         for (int idx = threadIdx.x; out && idx < 16 * MQ * D; idx += 256) {
             const int qrow = z * 16 * MQ + idx / D, d = idx % D;
@@ -411,7 +410,7 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     if (ctx > r.max_ctx) ctx = r.max_ctx;
     // rows (b, i >= nlive) are padding: neither cached nor flagged
     const int nlive = r.lim ? min(r.n, max(__builtin_amdgcn_readfirstlane(r.lim[b]), 0)) : r.n;
-    if (fused && c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0 && nlive > 0 &&
+    if (c == 0 && z == 0 && kvh == 0 && threadIdx.x == 0 && nlive > 0 &&
         (basepos < 0 || basepos + nlive > r.max_ctx))
         flag_error(r.err, ERR_CTX);                 // a live row's position outside [0, max_ctx)
     // the sequence's ceil(ctx / ch) chunks (the count k_attn_combine reads)
@@ -578,10 +577,10 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
 
     // two register sets: the next block's K and V load while this one computes
     u32x4 kf0[2][KS], kf1[2][KS], vv0[CPP / 2], vv1[CPP / 2];
-    // fused: a wave whose first block holds no new row loads it during the pass below
-    const bool early = fused && wq0 + 32 <= basepos;
-    if (!fused || early) load_kv(wq0, kf0, vv0);
-    // fused: one pass of the work-group over (a) its 16 MQ query rows, rotated,
+    // a wave whose first block holds no new row loads it during the pass below
+    const bool early = wq0 + 32 <= basepos;
+    if (early) load_kv(wq0, kf0, vv0);
+    // one pass of the work-group over (a) its 16 MQ query rows, rotated,
     // scaled and rounded to bf16 into LDS (the V tiles' space, unused until the
     // first block) and (b) its KV head's new rows [n0, p1), K rotated and V,
     // stored to the cache.  A task is 4 columns and their RoPE partners D/2
@@ -589,7 +588,7 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
     // memory round trip or two before the K/V stream starts.
     uint16_t* qst = &Vs[0][0];                                  // [16 MQ][D]
     static_assert(16 * MQ * D <= 4 * 32 * LDV, "query rows fit the V tiles");
-    if (fused) {
+    {
         constexpr int QG = D / 8;                               // 4-column groups of a half row
         const int n0 = max(p0, basepos), nkv = max(p1 - n0, 0);
         // tasks: the tile's live query rows, then the new K/V rows, then the
@@ -658,37 +657,19 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, co
         if (nkv > 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the new rows are stored before any wave reads them
         __syncthreads();                                        // and the query rows are in LDS
     }
-    if (fused && !early) load_kv(wq0, kf0, vv0);
-    // rows past QR read row 0 and are zeroed
+    if (!early) load_kv(wq0, kf0, vv0);
+    // the query fragments from LDS (rows past QR are zeros)
 #pragma unroll
     for (int mt = 0; mt < MQ; ++mt) {
         const int qrow = qbase + 16 * mt + lr;
         const bool live = qrow < QR;
-        const int qr = live ? qrow : 0;
-        const int g = qr / r.n, i = qr - g * r.n;
+        const int i = (live ? qrow : 0) % r.n;
         lim[mt] = live ? basepos + i : -1;
-        if (fused) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                qf[mt][ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qst + (16 * mt + lr) * D + 8 * (4 * ks + cq)));
-            continue;
-        }
-        const float sc = live ? qscale : 0.f;
-        const float4* qp = (const float4*)(q + ((size_t)(b * r.n + i) * n_q + kvh * G + g) * D);
-        float4 qv[KS][2];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            qv[ks][0] = qp[2 * (4 * ks + cq)];
-            qv[ks][1] = qp[2 * (4 * ks + cq) + 1];
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const float4 a = qv[ks][0], c2 = qv[ks][1];
-            qf[mt][ks] = __builtin_bit_cast(bf16x8, (u32x4){pack_bf16x2(a.x * sc, a.y * sc), pack_bf16x2(a.z * sc, a.w * sc),
-                                                            pack_bf16x2(c2.x * sc, c2.y * sc), pack_bf16x2(c2.z * sc, c2.w * sc)});
-        }
+        for (int ks = 0; ks < KS; ++ks)
+            qf[mt][ks] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qst + (16 * mt + lr) * D + 8 * (4 * ks + cq)));
     }
-    if (fused) lds_barrier();                                   // every wave holds its q before the V tiles take the space
+    lds_barrier();                                              // every wave holds its q before the V tiles take the space
 
     if constexpr (MQ == 2) {
         // one register set (246 VGPRs instead of 366): two waves per SIMD, the
@@ -950,14 +931,13 @@ static void launch_ev(F kern, dim3 grid, dim3 block, hipStream_t s, hipEvent_t e
 
 template <int D, bool PAGED>
 static void attn_mfma_launch(int MQ, dim3 grid, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, const rows_t& r,
-                             const float* q, int n_q, const cache_t& c, int layer, float* part, int mch, int ch,
-                             void* out, int out_t, qkv_src qs)
+                             int n_q, const cache_t& c, int layer, float* part, int mch, int ch, void* out, int out_t,
+                             qkv_src qs)
 {
     const uint16_t* kc = (const uint16_t*)c.k;
     const uint16_t* vc = (const uint16_t*)c.v;
     auto go = [&](auto kern) {
-        launch_ev(kern, grid, dim3(256), s, ev0, ev1, r, q, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t,
-                  qs);
+        launch_ev(kern, grid, dim3(256), s, ev0, ev1, r, n_q, c.n_kv, kc, vc, c.g, layer, part, mch, ch, out, out_t, qs);
     };
     switch (MQ) {
         case 1: go(k_attn_mfma<D, 1, PAGED>); break;
@@ -990,8 +970,8 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
         dim3 grid(r.B * c.n_kv, mch, zs);
         // one chunk per sequence: the kernel writes the final output itself
         void* o = mch == 1 ? out : nullptr;
-        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t, qs);
-        else attn_mfma_launch<D, false>(MQ, grid, s, ev0, ev1, r, q, n_q, c, layer, part, mch, ch, o, out_t, qs);
+        if (c.g.bt) attn_mfma_launch<D, true>(MQ, grid, s, ev0, ev1, r, n_q, c, layer, part, mch, ch, o, out_t, qs);
+        else attn_mfma_launch<D, false>(MQ, grid, s, ev0, ev1, r, n_q, c, layer, part, mch, ch, o, out_t, qs);
         return attn_split{mch, ch, o != nullptr};
     } else {
         dim3 grid(r.B * c.n_kv, max_chunks);
@@ -1001,15 +981,11 @@ static attn_split attn_t(const rows_t& r, const float* q, int n_q, const cache_t
     }
 }
 
-attn_split launch_attention(const rows_t& r, const float* q, int n_q, const cache_t& c, int layer, float* part,
-                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
-                            qkv_src qs)
+attn_split launch_attention(const rows_t& r, qkv_src qs, float* q, int n_q, const cache_t& c, int layer, float* part,
+                            int max_chunks, void* out, act_t out_t, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1)
 {
-    // the fp32 cache's kernel reads rotated queries: k_rope_kv runs first (into q)
-    if (c.kv_f32 && qs.rope) {
-        launch_rope_kv(r, qs.qkv, qs.P, qs.S, qs.rope, n_q, c, layer, const_cast<float*>(q), s);
-        qs = qkv_src{};
-    }
+    // the fp32 cache's kernel reads rotated queries: k_rope_kv writes them (and the new K/V rows) first
+    if (c.kv_f32) launch_rope_kv(r, qs.qkv, qs.P, qs.S, qs.rope, n_q, c, layer, q, s);
     if (c.head_dim == 128) {
         if (c.kv_f32) return attn_t<float, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
         return attn_t<uint16_t, 128>(r, q, n_q, c, layer, part, max_chunks, out, out_t, s, ev0, ev1, qs);
