@@ -365,7 +365,8 @@ __global__ void __launch_bounds__(256) k_attn_partial(rows_t r, const float* q, 
 #endif
 
 // two waves per SIMD where the registers allow it without spills (one query
-// tile; two tiles with a single K/V register set); three or four tiles keep one
+// tile; two tiles with a single K/V register set); three or four tiles run one
+// wave per SIMD
 //
 // RoPE and the cache write of the new rows are part of the kernel: from the
 // QKV projection's output (qkv_src, kernels.h) each work-group forms its
@@ -671,9 +672,12 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
     }
     lds_barrier();                                              // every wave holds its q before the V tiles take the space
 
-    if constexpr (MQ == 2) {
-        // one register set (246 VGPRs instead of 366): two waves per SIMD, the
-        // other wave hides each block's loads
+    if constexpr (MQ == 2 || MQ == 4) {
+        // one register set: with two tiles 246 VGPRs instead of 366, so two
+        // waves per SIMD and the other wave hides each block's loads; with four
+        // tiles the second set would spill (the 32B verify at gamma 9 took 822
+        // against 500 us per launch).  Three tiles keep both sets at one wave
+        // per SIMD (384 against 425 us at gamma 7).
         for (int blk = wq0; blk < wq1; blk += wstep) {
             if (blk != wq0) load_kv(blk, kf0, vv0);
             block(blk, kf0, vv0);
