@@ -21,6 +21,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -76,12 +77,20 @@ SOURCES_OF_CLASS = {
 }
 
 
+def _code_only(text):
+    """Source text with comments removed and whitespace collapsed, so that
+    only a change to the code itself changes the hash."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_sources_hash(files=None):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_18967_amd", "csrc")
     for f in sorted(files or os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(f.encode() + _code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -430,8 +430,8 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
 
     const float qscale = 1.4426950408889634f * rsqrtf((float)D);
 
-    // Q^T fragments (B operand of S^T = K Q^T), filled after the first K/V
-    // loads are issued so that the two memory round trips overlap
+    // Q^T fragments (B operand of S^T = K Q^T), read from LDS after the
+    // pass below has formed the rotated query rows
     bf16x8 qf[MQ][KS];
     int lim[MQ];
 
