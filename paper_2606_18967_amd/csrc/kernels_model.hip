@@ -754,34 +754,35 @@ __global__ void k_attn_combine(rows_t r, int n_q, int D, const float* part, int 
     int nch = (ctx + chunk - 1) / chunk;
     if (nch > max_chunks) nch = max_chunks;
     const float* pp = part + ((size_t)row * n_q + hq) * max_chunks * (D + 2);
-    // chunks are merged in order; the loads of eight chunks go out together
-    // (past the last chunk they repeat chunk nch - 1 and are not used)
+    // chunks are merged in order, sixteen at a time: the loads of a batch go
+    // out together (past the last chunk they repeat chunk nch - 1 and are not
+    // used), and a later batch with a larger maximum rescales the sums so far.
+    // Up to sixteen chunks this is one memory round trip and the same
+    // arithmetic as taking the maximum first.
+    constexpr int CB = 16;
     for (int k = threadIdx.x; k < D; k += blockDim.x) {
-        float mm = -INFINITY;
-        for (int c0 = 0; c0 < nch; c0 += 8) {
-            float cm[8], cl[8];
+        float mm = -INFINITY, ls = 0.f, os = 0.f;
+        for (int c0 = 0; c0 < nch; c0 += CB) {
+            float cm[CB], cl[CB], co[CB];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const float* pc = pp + (size_t)min(c0 + u, nch - 1) * (D + 2);
-                cm[u] = pc[0];
-                cl[u] = pc[1];
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (c0 + u < nch && cl[u] > 0.f) mm = fmaxf(mm, cm[u]);
-        }
-        float ls = 0.f, os = 0.f;
-        for (int c0 = 0; c0 < nch; c0 += 8) {
-            float cm[8], cl[8], co[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < CB; ++u) {
                 const float* pc = pp + (size_t)min(c0 + u, nch - 1) * (D + 2);
                 cm[u] = pc[0];
                 cl[u] = pc[1];
                 co[u] = pc[2 + k];
             }
+            float bm = mm;
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
+            for (int u = 0; u < CB; ++u)
+                if (c0 + u < nch && cl[u] > 0.f) bm = fmaxf(bm, cm[u]);
+            if (bm > mm && mm > -INFINITY) {
+                const float f = __expf(mm - bm);
+                ls *= f;
+                os *= f;
+            }
+            mm = bm;
+#pragma unroll
+            for (int u = 0; u < CB; ++u)
                 if (c0 + u < nch && cl[u] > 0.f) {
                     const float f = __expf(cm[u] - mm);
                     ls += cl[u] * f;
