@@ -468,13 +468,34 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
     __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)V, 0, ctx * D * 2, 0x00020000);
     const int koff = (lr * D + 8 * cq) * 2;                         // + (16 pt) D 2 + 64 ks
     const int voff = ((lane / CPP) * D + (lane % CPP) * 8) * 2;     // + t (64 / CPP) D 2
+    // Paged cache: the pages of the wave's blocks wq0 + k wstep for k in
+    // [kw, kw + 128), lane l holding those of k = kw + l and kw + 64 + l
+    // (-1: missing), loaded together when a block leaves the window, which
+    // also raises ERR_PAGE for a missing page of the wave's range.  A block
+    // then finds its page with a lane read: a table load or a flag store per
+    // block would make the compiler wait for every load in flight (they
+    // complete in order) before the next block's loads go out.
+    int pgw[2] = {-1, -1}, kw = -(1 << 20);
     auto load_kv = [&](int blk, u32x4 (&kf)[2][KS], u32x4 (&vv)[CPP / 2]) {
         int sb = __builtin_amdgcn_readfirstlane(blk * D * 2);         // scalar offset of the block
         if constexpr (PAGED) {
             const int lp = __builtin_amdgcn_readfirstlane(blk / kg.P), in0 = lp * kg.P;
-            long long pg = kv_page(kg, slot, lp);
-            pg = __builtin_amdgcn_readfirstlane((int)pg);
-            if (pg < 0 && lane == 0 && blk < ctx) flag_error(r.err, ERR_PAGE);
+            const int k = __builtin_amdgcn_readfirstlane((blk - wq0) / wstep);
+            if (k < kw || k >= kw + 128) {
+                kw = k;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int bj = wq0 + (k + 64 * h + lane) * wstep;
+                    pgw[h] = (int)kv_page(kg, slot, bj / kg.P);
+                    if (pgw[h] < 0 && bj < wq1)     // a global, not a generic, store: see above
+                        ((volatile __attribute__((address_space(1))) uint32_t*)r.err)[ERR_PAGE] = 1u;
+                }
+            }
+            const int j = k - kw;
+            // two lane reads and a scalar select: a vector select would need a
+            // temporary register, which may be one a load in flight still writes
+            const int pa = __builtin_amdgcn_readlane(pgw[0], j & 63), pb = __builtin_amdgcn_readlane(pgw[1], j & 63);
+            const int pg = j < 64 ? pa : pb;
             const int nrec = pg < 0 ? 0 : max(0, min(kg.P, ctx - in0)) * D * 2;
             const long long po = (pg < 0 ? 0 : pg) * kg.PS;
             krs = __builtin_amdgcn_make_buffer_rsrc((void*)(K + po), 0, nrec, 0x00020000);
