@@ -94,8 +94,12 @@ __global__ void __launch_bounds__(1024) k_embed_rmsnorm(rows_t r, const int32_t*
     }
 }
 
-// h[row] += sum_s P[s][row] (S > 1);  out[row] = RMSNorm(h[row]) * gain
-template <typename G, typename O>
+// h[row] += sum_s P[s][row] (S > 1);  out[row] = RMSNorm(h[row]) * gain.
+// Thread t holds the float4s t + j blockDim (j < NPT) of its row in registers:
+// the residual, the split-K partials and the gain are all requested before any
+// store, so a row costs one memory round trip and the block sum (a short row
+// batch runs on few CUs and is bound by that latency, not by its bytes).
+template <typename G, typename O, int NPT>
 __global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, int S, int R, int H, const G* gain,
                                                      float eps, void* out)
 {
@@ -103,21 +107,50 @@ __global__ void __launch_bounds__(1024) k_add_rmsnorm(float* h, const float* P, 
     const int row = blockIdx.x;
     float* hr = h + (size_t)row * H;
     const size_t RH = (size_t)R * H;
+    // a thread's float4s past the row end read the last one (in bounds) and are dropped
+    int kc[NPT];
+    float4 x[NPT], g[NPT];
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+        kc[j] = min((int)(threadIdx.x + j * blockDim.x) * 4, H - 4);
+        x[j] = *(const float4*)(hr + kc[j]);
+        g[j] = load4<G>(gain + kc[j]);
+    }
+    // the partials of all NPT float4s in batches of SB splits, each batch's
+    // loads together (a select, not a branch, drops the clamped repeats past
+    // S, so that no load is deferred into a branch of its own)
+    constexpr int SB = NPT <= 2 ? 8 : 16 / NPT;
+    const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; S > 1 && s0 < S; s0 += SB) {
+        float4 p[NPT][SB];
+#pragma unroll
+        for (int j = 0; j < NPT; ++j)
+#pragma unroll
+            for (int u = 0; u < SB; ++u)
+                p[j][u] = *(const float4*)(P + (size_t)min(s0 + u, S - 1) * RH + (size_t)row * H + kc[j]);
+#pragma unroll
+        for (int j = 0; j < NPT; ++j)
+#pragma unroll
+            for (int u = 0; u < SB; ++u) x[j] = add4(x[j], s0 + u < S ? p[j][u] : z4);
+    }
     float ss = 0.f;
-    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
-        float4 x = *(const float4*)(hr + k4);
-        if (S > 1) {
-            x = add_splits(x, P, S, RH, (size_t)row * H + k4);
-            *(float4*)(hr + k4) = x;
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+        const int k4 = (threadIdx.x + j * blockDim.x) * 4;
+        if (k4 < H) {
+            if (S > 1) *(float4*)(hr + k4) = x[j];
+            ss += x[j].x * x[j].x + x[j].y * x[j].y + x[j].z * x[j].z + x[j].w * x[j].w;
         }
-        ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
     }
     ss = block_sum(ss, red);
     const float inv = rsqrtf(ss / (float)H + eps);
-    for (int k4 = threadIdx.x * 4; k4 < H; k4 += blockDim.x * 4) {
-        const float4 x = *(const float4*)(hr + k4);
-        const float4 g = load4<G>(gain + k4);
-        store_act4<O>(out, (size_t)row * H + k4, make_float4(x.x * inv * g.x, x.y * inv * g.y, x.z * inv * g.z, x.w * inv * g.w));
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+        const int k4 = (threadIdx.x + j * blockDim.x) * 4;
+        if (k4 < H)
+            store_act4<O>(out, (size_t)row * H + k4,
+                          make_float4(x[j].x * inv * g[j].x, x[j].y * inv * g[j].y, x[j].z * inv * g[j].z,
+                                      x[j].w * inv * g[j].w));
     }
 }
 
@@ -909,14 +942,26 @@ void launch_embed_rmsnorm(const rows_t& r, const int32_t* tokA, int sA, const in
     else embed_norm_t(r, tokA, sA, tokB, sB, (const uint16_t*)E, H, V, h, (const uint16_t*)gain, eps, out, out_t, s);
 }
 
+template <typename G, int NPT>
+static void add_rmsnorm_n(float* h, const float* P, int S, int R, int H, const G* g, float eps, void* out, act_t t,
+                          hipStream_t s)
+{
+    const int th = ((H / 4 + NPT - 1) / NPT + 63) & ~63;      // <= 1024 by the caller's choice of NPT
+    if (t == ACT_F32) k_add_rmsnorm<G, float, NPT><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+    else if (t == ACT_BF16) k_add_rmsnorm<G, uint16_t, NPT><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+    else k_add_rmsnorm<G, _Float16, NPT><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+}
+
+// the fewest float4s per thread that cover the row with at most 1024 threads
+// (hidden <= 32768, which the engine's configuration check guarantees)
 template <typename G>
 static void add_rmsnorm_t(float* h, const float* P, int S, int R, int H, const G* g, float eps, void* out, act_t t,
                           hipStream_t s)
 {
-    const int th = H >= 4096 ? 1024 : 256;
-    if (t == ACT_F32) k_add_rmsnorm<G, float><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
-    else if (t == ACT_BF16) k_add_rmsnorm<G, uint16_t><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
-    else k_add_rmsnorm<G, _Float16><<<R, th, 0, s>>>(h, P, S, R, H, g, eps, out);
+    if (H <= 4 * 1024) add_rmsnorm_n<G, 1>(h, P, S, R, H, g, eps, out, t, s);
+    else if (H <= 8 * 1024) add_rmsnorm_n<G, 2>(h, P, S, R, H, g, eps, out, t, s);
+    else if (H <= 16 * 1024) add_rmsnorm_n<G, 4>(h, P, S, R, H, g, eps, out, t, s);
+    else add_rmsnorm_n<G, 8>(h, P, S, R, H, g, eps, out, t, s);
 }
 
 void launch_add_rmsnorm(float* h, const float* P, int S, int R, int H, const void* gain, int g_f32, float eps,
