@@ -509,8 +509,10 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
     // block would make the compiler wait for every load in flight (they
     // complete in order) before the next block's loads go out.
     int pgw[2] = {-1, -1}, kw = -(1 << 20);
-    auto load_kv = [&](int blk, u32x4 (&kf)[2][KS], u32x4 (&vv)[CPP / 2]) {
-        int sb = __builtin_amdgcn_readfirstlane(blk * D * 2);         // scalar offset of the block
+    int sb = 0;                                                     // scalar offset of the block
+    // the resources and offset of block blk, then its K and its V loads
+    auto kv_setup = [&](int blk) {
+        sb = __builtin_amdgcn_readfirstlane(blk * D * 2);
         if constexpr (PAGED) {
             const int lp = __builtin_amdgcn_readfirstlane(blk / kg.P), in0 = lp * kg.P;
             const int k = __builtin_amdgcn_readfirstlane((blk - wq0) / wstep);
@@ -535,21 +537,40 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
             vrs = __builtin_amdgcn_make_buffer_rsrc((void*)(V + po), 0, nrec, 0x00020000);
             sb = __builtin_amdgcn_readfirstlane((blk - in0) * D * 2);
         }
+    };
+    // no block: resources of zero records, whose loads return zeros without
+    // touching memory (so that a wave's loads need not sit in a branch)
+    auto kv_none = [&] {
+        sb = 0;
+        krs = __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0, 0x00020000);
+        vrs = __builtin_amdgcn_make_buffer_rsrc((void*)V, 0, 0, 0x00020000);
+    };
+    auto issue_k = [&](u32x4 (&kf)[2][KS]) {
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
                 kf[pt][ks] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                                            krs, koff + (16 * pt * D + 32 * ks) * 2, sb, ATT_NT));
+    };
+    auto issue_v = [&](u32x4 (&vv)[CPP / 2]) {
 #pragma unroll
         for (int t = 0; t < CPP / 2; ++t)
             vv[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                                   vrs, voff + t * (64 / CPP) * D * 2, sb, ATT_NT));
     };
+    auto load_kv = [&](int blk, u32x4 (&kf)[2][KS], u32x4 (&vv)[CPP / 2]) {
+        kv_setup(blk);
+        issue_k(kf);
+        issue_v(vv);
+    };
     // lane l's pieces of the transposing LDS reads that build V^T fragments:
     // positions 4*(l/16) + (l%16)/4 (+16), dims 4*(l%4) of each 16-dim block
     const int trow = 4 * cq + (lr >> 2), tcol = 4 * (lr & 3);
-    auto block = [&](int blk, const u32x4 (&kf)[2][KS], const u32x4 (&vv)[CPP / 2]) {
+    // after_k runs once the block's K fragments are consumed (after the last
+    // tile's S^T products), after_v once its V is in LDS: a single register
+    // set requests the next block's K and V there
+    auto block = [&](int blk, const u32x4 (&kf)[2][KS], const u32x4 (&vv)[CPP / 2], auto after_k, auto after_v) {
         bf16x8 pf[MQ];
 #pragma unroll
         for (int mt = 0; mt < MQ; ++mt) {
@@ -562,6 +583,7 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
                     st[pt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[pt][ks]), qf[mt][ks],
                                                                      st[pt], 0, 0, 0);
             }
+            if (mt == MQ - 1) after_k();
             float bm = -INFINITY;
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt)
@@ -609,6 +631,7 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
             const int pos = piece / CPP, ch = piece - pos * CPP;
             *(u32x4*)(vs + pos * LDV + ch * 8) = vv[t];
         }
+        after_v();
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -732,17 +755,29 @@ __global__ void __launch_bounds__(256, MQ <= 2 ? 2 : 1) k_attn_mfma(rows_t r, in
         // tiles the second set would spill (the 32B verify at gamma 9 took 822
         // against 500 us per launch).  Three tiles keep both sets at one wave
         // per SIMD (384 against 425 us at gamma 7).
+        // The next block's K loads go out once this block's S^T products have
+        // read K, its V loads once this block's V is in LDS; after the wave's
+        // last block they read nothing.  Issued in a branch, they would make
+        // the compiler wait for them wherever the paths join.
         for (int blk = wq0; blk < wq1; blk += wstep) {
-            if (blk != wq0) load_kv(blk, kf0, vv0);
-            block(blk, kf0, vv0);
+            const int nx = blk + wstep;
+            block(
+                blk, kf0, vv0,
+                [&] {
+                    if (nx < wq1) kv_setup(nx);
+                    else kv_none();
+                    issue_k(kf0);
+                },
+                [&] { issue_v(vv0); });
         }
     } else {
+        const auto none = [] {};
         for (int blk = wq0; blk < wq1; blk += 2 * wstep) {
             load_kv(blk + wstep, kf1, vv1);
-            block(blk, kf0, vv0);
+            block(blk, kf0, vv0, none, none);
             if (blk + wstep >= wq1) break;
             load_kv(blk + 2 * wstep, kf0, vv0);
-            block(blk + wstep, kf1, vv1);
+            block(blk + wstep, kf1, vv1, none, none);
         }
     }
 #pragma unroll
