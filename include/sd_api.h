@@ -98,7 +98,9 @@ int32_t sd_num_weights(const sd_model_cfg* cfg);
  *   [2] LM head [vocab][hidden], then per layer l (base 3 + 6*l):
  *   attn-norm gain [hidden], Wqkv [(n_q+2*n_kv)*head_dim][hidden] (rows: Wq,
  *   then Wk, then Wv), Wo [hidden][n_q*head_dim], ffn-norm gain [hidden],
- *   Wgu [2*ffn][hidden] (rows: gate, then up), Wdown [hidden][ffn]. */
+ *   Wgu [2*ffn][hidden] (rows: gate, then up), Wdown [hidden][ffn].
+ * Every pointer must be 16-byte aligned (the kernels read weights in
+ * 16-byte pieces); a NULL or misaligned pointer gives SD_E_INVAL. */
 sd_status sd_bind_weights(sd_engine e, const void* const* tensors, int32_t n);
 
 /* Bytes of EACH of the K and V caches: n_layers*max_slots*n_kv*max_ctx*

@@ -322,8 +322,10 @@ extern "C" sd_status sd_bind_weights(sd_engine e, const void* const* t, int32_t 
 {
     if (!e || !t) return fail(SD_E_INVAL, "NULL argument");
     if (n != sd_num_weights(&e->c)) return fail(SD_E_INVAL, "expected %d tensors, got %d", sd_num_weights(&e->c), n);
-    for (int i = 0; i < n; ++i)
+    for (int i = 0; i < n; ++i) {
         if (!t[i]) return fail(SD_E_INVAL, "tensor %d is NULL", i);
+        if ((uintptr_t)t[i] & 15) return fail(SD_E_INVAL, "tensor %d is not 16-byte aligned", i);
+    }
     for (int i = 0; i < n; ++i) e->w[i] = t[i];
     e->weights_bound = true;
     e->drafter_ready = false;   // quantized copy is stale until refreshed

@@ -152,6 +152,13 @@ def test_device_range_errors_are_reported(cfg):
     with pytest.raises((sdrl.SDError, ValueError)):
         eng.draft(i32([0]), i32([1]), 0, 1.0, 0, 0, torch.zeros((1, 0), dtype=torch.int32, device="cuda"),
                   torch.zeros((1, 0, cfg["vocab"]), device="cuda"), torch.zeros((1, 0, 2), device="cuda"))
+    # weights must be 16-byte aligned (a contiguous view one element into a buffer is not)
+    buf = torch.zeros(W[1].numel() + 8, dtype=W[1].dtype, device="cuda")
+    off = list(W)
+    off[1] = buf[1:1 + W[1].numel()].view(W[1].shape)
+    with pytest.raises(sdrl.SDError, match="aligned"):
+        eng.bind_weights(off)
+    eng.bind_weights(W)
     kv_len.zero_()
     eng.sync()
     eng.close()
