@@ -109,7 +109,8 @@ size_t sd_kv_bytes(const sd_model_cfg* cfg, int32_t max_slots, int32_t max_ctx);
 
 /* Binds the shared KV cache (App. D.1: the drafter writes provisional
  * entries into the target's cache) and the per-slot lengths kv_len
- * (device int32[max_slots]).  K holds post-RoPE keys. */
+ * (device int32[max_slots]).  K holds post-RoPE keys.  k and v must be
+ * 16-byte aligned (SD_E_INVAL otherwise). */
 sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len);
 
 /* Bytes of EACH of the K and V pages of a paged cache: n_layers*n_kv*
@@ -126,8 +127,8 @@ size_t sd_kv_page_bytes(const sd_model_cfg* cfg, int32_t page_size);
  * hand pages of finished sequences to new ones) but not while a call it
  * enqueued is running.  Positions are still kv_len-relative: rollback only
  * moves kv_len, and pages past it stay the caller's to reuse.  Requires
- * page_size a multiple of 32 and pages_per_seq*page_size >= max_ctx
- * (SD_E_INVAL otherwise).  A table entry outside [0, n_pages) met on the
+ * page_size a multiple of 32, pages_per_seq*page_size >= max_ctx and
+ * 16-byte aligned pools (SD_E_INVAL otherwise).  A table entry outside [0, n_pages) met on the
  * device is skipped and reported by sd_sync as SD_E_INVAL.  Replaces any
  * earlier binding. */
 sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages, int32_t n_pages, int32_t page_size,

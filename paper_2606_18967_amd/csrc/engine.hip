@@ -335,6 +335,7 @@ extern "C" sd_status sd_bind_weights(sd_engine e, const void* const* t, int32_t 
 extern "C" sd_status sd_bind_kv(sd_engine e, void* k, void* v, int32_t* kv_len)
 {
     if (!e || !k || !v || !kv_len) return fail(SD_E_INVAL, "NULL argument");
+    if (((uintptr_t)k | (uintptr_t)v) & 15) return fail(SD_E_INVAL, "k and v must be 16-byte aligned");
     e->k = k;
     e->v = v;
     e->kv_len = kv_len;
@@ -354,6 +355,8 @@ extern "C" sd_status sd_bind_kv_paged(sd_engine e, void* k_pages, void* v_pages,
                                       const int32_t* block_table, int32_t pages_per_seq, int32_t* kv_len)
 {
     if (!e || !k_pages || !v_pages || !block_table || !kv_len) return fail(SD_E_INVAL, "NULL argument");
+    if (((uintptr_t)k_pages | (uintptr_t)v_pages) & 15)
+        return fail(SD_E_INVAL, "k_pages and v_pages must be 16-byte aligned");
     if (n_pages < 1 || page_size < 32 || page_size % 32)
         return fail(SD_E_INVAL, "need n_pages >= 1 and page_size a positive multiple of 32 (got %d, %d)", n_pages,
                     page_size);

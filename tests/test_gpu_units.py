@@ -159,6 +159,11 @@ def test_device_range_errors_are_reported(cfg):
     with pytest.raises(sdrl.SDError, match="aligned"):
         eng.bind_weights(off)
     eng.bind_weights(W)
+    # so must the cache
+    kb = torch.zeros(k.numel() + 8, dtype=k.dtype, device="cuda")
+    with pytest.raises(sdrl.SDError, match="aligned"):
+        eng.bind_kv(kb[1:1 + k.numel()].view(k.shape), v, kv_len)
+    eng.bind_kv(k, v, kv_len)
     kv_len.zero_()
     eng.sync()
     eng.close()
