@@ -2,13 +2,15 @@
 
 The bf16 attention kernel takes a KV head's (n_q / n_kv) * (gamma + 1) query
 rows in 16-row tiles, one to four per work-group (k_attn_mfma<D, MQ>), with
-two K/V register sets at one and three tiles and one set at two and four.
+two K/V register sets at one and three tiles and one set at two and four
+(where the next block's loads, and on a paged cache its page lookup, go out
+in the middle of the block).
 On a decoder with four query heads per KV head a verify at gamma = 3, 7, 11
 and 15 has 16, 32, 48 and 64 query rows per KV head: one, two, three and
 four tiles.  Each verify runs after 613-1017 positions of random context
 (two or three attention chunks with four sequences); every row's logits and
 the new cache rows are checked against the oracle's forward over the same
-tokens.
+tokens, on a dense cache and on shuffled pages of 64 positions.
 """
 import numpy as np
 import pytest
@@ -26,17 +28,18 @@ GQA4 = dict(name="gqa4-bf16", n_layers=2, hidden=512, n_q=4, n_kv=1, head_dim=12
             dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
 
 
+@pytest.mark.parametrize("page", [0, 64], ids=["dense", "paged"])
 @pytest.mark.parametrize("gamma", [3, 7, 11, 15], ids=["1tile", "2tiles", "3tiles", "4tiles"])
-def test_verify_every_query_tile_count_matches_oracle(gamma):
+def test_verify_every_query_tile_count_matches_oracle(gamma, page):
     cfg, seed, tol = GQA4, 31 + gamma, 2e-2
     B = 4
     lens = [700, 613, 941, 1017]
     max_ctx = max(lens) + gamma + 8
-    say("verify query tiles", gamma, (cfg["n_q"] // cfg["n_kv"]) * (gamma + 1), "rows per KV head")
+    say("verify query tiles", gamma, (cfg["n_q"] // cfg["n_kv"]) * (gamma + 1), "rows per KV head, page", page)
     W = synth.make_weights(cfg, seed, "cpu")
     eng = sdrl.Engine(cfg, B, max_ctx, gamma)
     eng.bind_weights([w.cuda() for w in W])
-    kv = DeviceKV(eng, max_ctx, 0, seed)
+    kv = DeviceKV(eng, max_ctx, page, seed)
     kv.fill_context(max(lens), seed + 100)
     kv.kv_len.copy_(i32(lens))
     eng.refresh_drafter()
