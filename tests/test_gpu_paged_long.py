@@ -26,11 +26,15 @@ pytestmark = pytest.mark.gpu
 
 WIDE = dict(name="wide-kv-bf16", n_layers=2, hidden=1024, n_q=8, n_kv=8, head_dim=128, ffn=1024, vocab=512,
             dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
+# four query heads per KV head: 20 query rows per KV head at gamma 4, two
+# 16-row tiles, the kernel whose next block (and page) is set up mid-block
+WIDE_G4 = dict(WIDE, name="wide-kv-gqa4-bf16", n_q=32)
 PAGE, WINDOW = 32, 128
 
 
-def test_paged_verify_past_the_page_window_matches_dense_and_oracle():
-    cfg, gamma, seed, tol = WIDE, 4, 41, 2e-2
+@pytest.mark.parametrize("cfg", [WIDE, WIDE_G4], ids=["1tile", "2tiles"])
+def test_paged_verify_past_the_page_window_matches_dense_and_oracle(cfg):
+    gamma, seed, tol = 4, 41, 2e-2
     B = 64
     # ragged: most contexts past the window of every wave, a few short ones
     lens = [3000 + 7 * b if b % 16 == 5 else 16500 + (53 * b) % 190 for b in range(B)]
