@@ -10,7 +10,9 @@ a context above 16480 positions makes every wave reload its window once.
 A verify over such contexts (page size 32, shuffled pages) must give the
 same logits and the same cache bit for bit as the dense cache, match the
 oracle on sampled sequences, and report a missing page that only the second
-window reaches.
+window reaches; with one query head per KV head (one query tile) and with
+four (two tiles, whose next block and its page are set up in the middle of
+the block).
 """
 import numpy as np
 import pytest
