@@ -10,7 +10,8 @@ and 15 has 16, 32, 48 and 64 query rows per KV head: one, two, three and
 four tiles.  Each verify runs after 613-1017 positions of random context
 (two or three attention chunks with four sequences); every row's logits and
 the new cache rows are checked against the oracle's forward over the same
-tokens, on a dense cache and on shuffled pages of 64 positions.
+tokens, on a dense cache and on shuffled pages of 64 positions, at head
+sizes 128 and 64.
 """
 import numpy as np
 import pytest
@@ -26,12 +27,15 @@ pytestmark = pytest.mark.gpu
 # four query heads per KV head at the production head size
 GQA4 = dict(name="gqa4-bf16", n_layers=2, hidden=512, n_q=4, n_kv=1, head_dim=128, ffn=1024, vocab=1024,
             dtype="bf16", rope_theta=500000.0, rms_eps=1e-5)
+# the same at the other head size the kernel is built for
+GQA4_D64 = dict(GQA4, name="gqa4-d64-bf16", head_dim=64)
 
 
+@pytest.mark.parametrize("cfg", [GQA4, GQA4_D64], ids=["d128", "d64"])
 @pytest.mark.parametrize("page", [0, 64], ids=["dense", "paged"])
 @pytest.mark.parametrize("gamma", [3, 7, 11, 15], ids=["1tile", "2tiles", "3tiles", "4tiles"])
-def test_verify_every_query_tile_count_matches_oracle(gamma, page):
-    cfg, seed, tol = GQA4, 31 + gamma, 2e-2
+def test_verify_every_query_tile_count_matches_oracle(gamma, page, cfg):
+    seed, tol = 31 + gamma, 2e-2
     B = 4
     lens = [700, 613, 941, 1017]
     max_ctx = max(lens) + gamma + 8
